@@ -1,0 +1,144 @@
+"""Seeded synthetic workloads shaped like the paper's video-DiT attention.
+
+This module only draws inputs: shapes, seeds and random tensors. It holds none
+of the method's arithmetic and imports neither the HIP library nor the oracle,
+so both sides of every parity check can take their inputs from it.
+
+The paper measured Wan2.1-T2V-1.3B (21 latent frames x 3,600 tokens, 12 heads,
+head_dim 128), CogVideoX-v1.5 and HunyuanVideo on a prompt benchmark (Sec. 4).
+No weights or prompts are available here, so Q/K/V and latents are i.i.d.
+normal draws with the shapes of those workloads:
+
+  tiny     T=5  x 8x8   (320 tokens),     2 heads, d=64,  fp32, keyframes {0,2,4}
+  small    T=13 x 30x52 (20,280 tokens), 12 heads, d=128, bf16, Q/K/V scaled by
+           1/sqrt(128), keyframes every 3rd frame {0,3,6,9,12}
+  480p     T=21 x 30x52 (32,760 tokens), 12 heads, d=128, bf16, 6 evenly spaced
+           keyframes including first and last {0,4,8,12,16,20}
+  720p     T=21 x 45x80 (75,600 tokens, the Wan2.1 720p grid), 40 heads,
+           d=128, bf16, first frame + every 4th {0,4,8,12,16,20}
+  long     T=33 x 45x80 (118,800 tokens), 24 heads, d=128, bf16, every 6th
+           frame {0,6,...,30} plus 2 extra keyframes drawn with
+           numpy.random.default_rng(4) from the remaining frames ({22, 31})
+
+Draw order: Q, K, V from one torch generator seeded with the workload's index
+(tiny 0 ... long 4), fp32 randn, times the workload's scale, then rounded to
+bf16 (round-to-nearest-even, torch's conversion) for the bf16 workloads.
+Latents: slot 0 then slot 1, fp32 randn from a generator seeded index + 100.
+Latent grids: tiny 4 x 5x16x16; 480p 16 x 21x60x104; the others 16 x T x 2H x 2W.
+Projection timesteps (t_start, t_end, tau) = (24, 21, 23), i.e. alpha = 1/3.
+"""
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    index: int
+    T: int
+    H: int
+    W: int
+    heads: int
+    head_dim: int
+    dtype: str                      # "f32" or "bf16"
+    keyframes: Tuple[int, ...]
+    qkv_scale: float
+    latent_c: int
+    latent_hw: Tuple[int, int]
+    timesteps: Tuple[float, float, float] = (24.0, 21.0, 23.0)
+    note: str = ""
+
+    @property
+    def N(self) -> int:
+        return self.H * self.W
+
+    @property
+    def S(self) -> int:
+        return self.T * self.H * self.W
+
+    @property
+    def M(self) -> int:
+        return len(self.keyframes)
+
+    @property
+    def torch_dtype(self):
+        return torch.float32 if self.dtype == "f32" else torch.bfloat16
+
+
+def _long_video_keyframes() -> Tuple[int, ...]:
+    base = list(range(0, 33, 6))
+    rest = [f for f in range(33) if f not in base]
+    extra = np.random.default_rng(4).choice(rest, 2, replace=False)
+    return tuple(sorted(base + [int(x) for x in extra]))
+
+
+WORKLOADS = {
+    "tiny": Workload("tiny", 0, 5, 8, 8, 2, 64, "f32", (0, 2, 4), 1.0, 4, (16, 16)),
+    "small": Workload("small", 1, 13, 30, 52, 12, 128, "bf16", (0, 3, 6, 9, 12),
+                      1.0 / np.sqrt(128.0), 16, (60, 104)),
+    "480p": Workload("480p", 2, 21, 30, 52, 12, 128, "bf16", (0, 4, 8, 12, 16, 20),
+                     1.0, 16, (60, 104)),
+    "720p": Workload("720p", 3, 21, 45, 80, 40, 128, "bf16", (0, 4, 8, 12, 16, 20),
+                     1.0, 16, (90, 160)),
+    "long": Workload("long", 4, 33, 45, 80, 24, 128, "bf16", _long_video_keyframes(),
+                     1.0, 16, (90, 160)),
+}
+ORDER = ["tiny", "small", "480p", "720p", "long"]
+
+
+def custom(T, H, W, heads, head_dim, keyframes, dtype="bf16", seed=0,
+           qkv_scale=1.0, name="custom") -> Workload:
+    """A workload of any shape (parity cases that span several tiles)."""
+    return Workload(name, seed, T, H, W, heads, head_dim, dtype, tuple(keyframes),
+                    qkv_scale, 4, (2 * H, 2 * W))
+
+
+def make_qkv(w: Workload, device="cpu", seed=None, scale=None):
+    """Q, K, V as [S][heads][head_dim] tensors on `device`."""
+    g = torch.Generator(device=device)
+    g.manual_seed(w.index if seed is None else seed)
+    s = w.qkv_scale if scale is None else scale
+    shape = (w.S, w.heads, w.head_dim)
+    out = []
+    for _ in range(3):
+        x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        if s != 1.0:
+            x.mul_(s)
+        out.append(x.to(w.torch_dtype))
+    return tuple(out)
+
+
+def make_latents(w: Workload, B=1, device="cpu", dtype=None, seed=None):
+    """Latents [B][2][C][T][Hl][Wl]: slot 0 and slot 1 are independent draws."""
+    g = torch.Generator(device=device)
+    g.manual_seed((w.index + 100) if seed is None else seed)
+    Hl, Wl = w.latent_hw
+    shape = (B, 2, w.latent_c, w.T, Hl, Wl)
+    x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    dt = torch.float32 if dtype is None else dtype
+    return x.to(dt)
+
+
+def sample_rows(w: Workload, per_head: int, tile: int = 128, seed: int = 1234):
+    """A seeded sample of compact query rows: every keyframe's first and last
+    row, rows on both sides of each `tile` boundary, the final row, and
+    random rows up to `per_head`."""
+    Mq = w.M * w.N
+    must = set()
+    for m in range(w.M):
+        must.add(m * w.N)
+        must.add(m * w.N + w.N - 1)
+    for b in range(tile, Mq, tile * max(1, (Mq // tile) // 8)):
+        must.add(b - 1)
+        must.add(b)
+    must.add(Mq - 1)
+    rng = np.random.default_rng(seed)
+    rows = sorted(r for r in must if 0 <= r < Mq)
+    extra = max(0, per_head - len(rows))
+    if extra:
+        pool = np.setdiff1d(np.arange(Mq), np.array(rows))
+        rows += rng.choice(pool, min(extra, pool.size), replace=False).tolist()
+    return np.array(sorted(rows), dtype=np.int64)
