@@ -1,0 +1,276 @@
+#!/usr/bin/env python3
+"""Benchmark of the keyframe-query attention path on one MI355X.
+
+One step is one pass of the hot path at a skip step over one batch of
+synthetic input already resident in HBM:
+  1. keyframe set normalisation and mask (host, C ABI),
+  2. latent trajectory projection of the non-keyframes (Eq. 3),
+  3. keyframe-query attention with the fused query gather,
+  4. scatter of the keyframe rows into the full-sequence output.
+The all-frame comparator (the same kernel with every frame a keyframe, i.e.
+the dense attention of warm-up steps and Rhythmic Points) is timed beside it
+for the speedup.
+
+Prints ONE JSON line. `value` is keyframe-query attention TFLOP per second of
+whole-step time; `roofline` describes the attention kernel alone, timed with
+HIP events around each launch on the stream it runs on.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "keyframe-query 3D attention TFLOP/s + % bf16 MFMA peak; speedup vs all-frame"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="long",
+                    help="long (default), 720p, 480p, small")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-comparator", action="store_true")
+    ap.add_argument("--no-bandwidth", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU work of the oracle baseline sample")
+    return ap.parse_args()
+
+
+def _events(n):
+    import torch
+    return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(n)]
+
+
+def _avg_ms(pairs):
+    return sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
+
+
+def cpu_baseline(w, q, k, v, target_s):
+    """The oracle as it stands, on a bounded sample of query rows."""
+    import numpy as np
+    import oracle
+    from paper_2606_06309_amd import accounting
+
+    qh, kh, vh = q.cpu(), k.cpu(), v.cpu()
+    rowmap = oracle.rowmap(w.keyframes, w.N)
+    rng = np.random.default_rng(2026)
+    cores = oracle.num_threads()
+
+    def run(n):
+        rows = rng.choice(rowmap.size, n, replace=True)
+        heads = rng.integers(0, w.heads, n)
+        t0 = time.perf_counter()
+        oracle.attention_pairs(qh, kh, vh, rowmap[rows], heads)
+        return time.perf_counter() - t0
+
+    n0 = max(2, cores)
+    t_cal = run(n0)
+    n = int(max(n0, min(200000, n0 * target_s / max(t_cal, 1e-3))))
+    t = run(n)
+    flop = n * accounting.attention_flops(1, w.S, w.head_dim, 1)
+    return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} random (keyframe row, head) pairs of the {w.name} workload, each over "
+                      f"all S={w.S} keys, fp64; {t:.1f} s"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}): "
+              "the keyframe-query attention path has no multi-GPU form in this build; "
+              "see DESIGN.md for how it would shard by head.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = workloads.WORKLOADS[args.workload]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    print(f"[bench] workload {w.name}: T={w.T} H={w.H} W={w.W} heads={w.heads} d={w.head_dim} "
+          f"M={w.M} keyframes={list(w.keyframes)}", file=sys.stderr, flush=True)
+
+    q, k, v = workloads.make_qkv(w, device=dev)
+    lat = workloads.make_latents(w, B=1, device=dev)
+    Hl, Wl = w.latent_hw
+    proj_out = torch.empty((1, w.latent_c, w.T, Hl, Wl), dtype=lat.dtype, device=dev)
+    Mq = w.M * w.N
+    attn_out = torch.empty((Mq, w.heads, w.head_dim), dtype=q.dtype, device=dev)
+    full_out = torch.zeros((w.S, w.heads, w.head_dim), dtype=q.dtype, device=dev)
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        ids, mask = rf.rf_select_keyframes(w.keyframes, w.T)
+        rf.rf_project_latents(lat, w.timesteps, mask, out=proj_out)
+        if ev is not None:
+            ev[0].record()
+        rf.rf_keyframe_attention(q, k, v, ids, w.T, w.H, w.W, out=attn_out)
+        if ev is not None:
+            ev[1].record()
+        rf.rf_scatter_frames(attn_out, full_out, ids, w.T, w.N)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = _events(args.steps)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        step(ev[i])
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / args.steps
+    attn_ms = _avg_ms(ev)
+    flop = accounting.attention_flops(Mq, w.S, w.head_dim, w.heads)
+    value = flop / (ms_step * 1e-3) / 1e12
+    attn_tflops = flop / (attn_ms * 1e-3) / 1e12
+    print(f"[bench] step {ms_step:.3f} ms, attention {attn_ms:.3f} ms = {attn_tflops:.1f} TFLOP/s",
+          file=sys.stderr, flush=True)
+
+    result = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded normal Q/K/V and latents; no model weights)",
+        "config": {"workload": w.name, "T": w.T, "H": w.H, "W": w.W, "tokens": w.S,
+                   "heads": w.heads, "head_dim": w.head_dim, "keyframes": list(w.keyframes),
+                   "query_rows": Mq, "latents": [1, w.latent_c, w.T, Hl, Wl],
+                   "latent_dtype": "f32", "parallelism": "none (1 GPU)"},
+        "attention": {"avg_ms": round(attn_ms, 4), "tflops": round(attn_tflops, 2),
+                      "frac_bf16_peak": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                      "flop_per_launch": flop},
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+    }
+
+    if not args.no_comparator:
+        all_out = torch.empty((w.S, w.heads, w.head_dim), dtype=q.dtype, device=dev)
+        all_ids = list(range(w.T))
+        rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=all_out)
+        torch.cuda.synchronize()
+        n_all = max(1, min(args.steps, 5))
+        ev_all = _events(n_all)
+        for i in range(n_all):
+            ev_all[i][0].record()
+            rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=all_out)
+            ev_all[i][1].record()
+        torch.cuda.synchronize()
+        all_ms = _avg_ms(ev_all)
+        all_flop = accounting.attention_flops(w.S, w.S, w.head_dim, w.heads)
+        result["all_frame"] = {"avg_ms": round(all_ms, 4),
+                               "tflops": round(all_flop / (all_ms * 1e-3) / 1e12, 2),
+                               "launches": n_all}
+        result["speedup_vs_all_frame"] = round(all_ms / attn_ms, 4)
+        result["ideal_speedup"] = round(accounting.ideal_speedup(w.T, w.M), 4)
+        del all_out
+        print(f"[bench] all-frame {all_ms:.3f} ms, speedup {all_ms / attn_ms:.3f} "
+              f"(ideal {w.T / w.M:.3f})", file=sys.stderr, flush=True)
+
+    if not args.no_bandwidth:
+        result["bandwidth"] = bandwidth(w, q, attn_out, full_out, args)
+
+    if not args.no_cpu_baseline:
+        print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+def bandwidth(w, q, attn_out, full_out, args):
+    """Projection and gather/scatter bandwidth. A single projection at the
+    workload's latent size fits in the 256 MB Infinity Cache, so the HBM rate
+    is taken on a batch of >= 1 GB per launch, rotating through 3 buffer sets
+    (each set larger than the cache); the single-launch latency is reported
+    beside it. Gather and scatter at this size already exceed the cache."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    dev = "cuda"
+    n = max(3, args.steps)
+    ids, mask = rf.rf_select_keyframes(w.keyframes, w.T)
+    Hl, Wl = w.latent_hw
+    plane = Hl * Wl
+    per_b = accounting.projection_bytes(1, w.latent_c, w.T, plane, w.M, 4)
+    B = max(1, -(-(1 << 30) // per_b))
+    sets = []
+    for s in range(3):
+        lat = workloads.make_latents(w, B=B, device=dev, seed=500 + s)
+        sets.append((lat, torch.empty((B, w.latent_c, w.T, Hl, Wl), dtype=lat.dtype, device=dev)))
+    for lat, out in sets:
+        rf.rf_project_latents(lat, w.timesteps, mask, out=out)
+    torch.cuda.synchronize()
+    ev = _events(n)
+    for i in range(n):
+        lat, out = sets[i % 3]
+        ev[i][0].record()
+        rf.rf_project_latents(lat, w.timesteps, mask, out=out)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    proj_ms = _avg_ms(ev)
+    proj_bytes = per_b * B
+    del sets
+
+    lat1 = workloads.make_latents(w, B=1, device=dev)
+    out1 = torch.empty((1, w.latent_c, w.T, Hl, Wl), dtype=lat1.dtype, device=dev)
+    rf.rf_project_latents(lat1, w.timesteps, mask, out=out1)
+    ev1 = _events(n)
+    for i in range(n):
+        ev1[i][0].record()
+        rf.rf_project_latents(lat1, w.timesteps, mask, out=out1)
+        ev1[i][1].record()
+    torch.cuda.synchronize()
+    single_ms = _avg_ms(ev1)
+
+    row_bytes = w.heads * w.head_dim * q.element_size()
+    g_bytes = accounting.gather_bytes(w.M, w.N, row_bytes)
+    dsts = [attn_out, torch.empty_like(attn_out)]
+    rf.rf_gather_frames(q, ids, w.T, w.N, out=dsts[0])
+    torch.cuda.synchronize()
+    evg = _events(n)
+    for i in range(n):
+        evg[i][0].record()
+        rf.rf_gather_frames(q, ids, w.T, w.N, out=dsts[i % 2])
+        evg[i][1].record()
+    evs = _events(n)
+    for i in range(n):
+        evs[i][0].record()
+        rf.rf_scatter_frames(dsts[i % 2], full_out, ids, w.T, w.N)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    g_ms, s_ms = _avg_ms(evg), _avg_ms(evs)
+
+    def rate(b, ms):
+        gbs = b / (ms * 1e-3) / 1e9
+        return {"bytes": b, "avg_us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
+                "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+
+    res = {"projection_batched": dict(rate(proj_bytes, proj_ms), batch=B, dtype="f32",
+                                      rotation_sets=3),
+           "projection_single": dict(rate(per_b, single_ms), batch=1, dtype="f32"),
+           "gather": rate(g_bytes, g_ms), "scatter": rate(g_bytes, s_ms)}
+    print(f"[bench] projection {res['projection_batched']['gbs']} GB/s (B={B}), single "
+          f"{res['projection_single']['avg_us']} us; gather {res['gather']['gbs']} GB/s, "
+          f"scatter {res['scatter']['gbs']} GB/s", file=sys.stderr, flush=True)
+    return res
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * rhymeflow.h -- C ABI of librhymeflow.so, the keyframe-query attention path
+ * of RhymeFlow (asynchronous frame scheduling for video DiTs, arXiv 2606.06309)
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * At a denoising step where only keyframes are updated, the keyframes' query
+ * tokens attend over the keys and values of every frame: the true states of
+ * keyframes and the projected states of the skipped non-keyframes
+ * (Sec. 3.2.3-3.2.4; App. B.2). This library provides the calls of that step:
+ * keyframe-set normalisation, the latent trajectory projection of Eq. (3),
+ * keyframe-query attention, and the frame gather/scatter around it.
+ *
+ * Conventions shared by every call:
+ *  - Return value: RF_OK (0) or a negative rf_status. No C++ exception crosses
+ *    this ABI. rf_last_error() gives a thread-local description of the last
+ *    failure on the calling thread.
+ *  - Every argument is validated before any HIP call, so a rejected call has
+ *    no effect on the device.
+ *  - Device buffers are owned by the caller, must stay alive until the stream
+ *    has passed the launched work, and are never retained by the library.
+ *    Host arrays are read during the call only; the caller may free them when
+ *    the call returns. The library allocates no memory.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Calls only enqueue
+ *    work; they do not synchronise. Device faults surface at the caller's next
+ *    synchronisation, not as a return code.
+ *  - Calls hold no global state and may be made from several threads.
+ *  - Device pointers must be 16-byte aligned (128-bit accesses), otherwise
+ *    RF_ERR_UNSUPPORTED.
+ */
+#ifndef RHYMEFLOW_H
+#define RHYMEFLOW_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RF_ABI_VERSION 1
+
+/* Largest number of frames T a call accepts (keyframe ids travel inside the
+   kernel arguments, which needs no device copy and no allocation). */
+#define RF_MAX_FRAMES 256
+
+typedef enum {
+    RF_OK = 0,
+    RF_ERR_INVALID_ARG = -1,  /* NULL pointer, size <= 0, bad id list, NaN time */
+    RF_ERR_UNSUPPORTED = -2,  /* valid request outside what the kernels cover */
+    RF_ERR_RANGE = -3,        /* an id or size outside its range */
+    RF_ERR_HIP = -4           /* the HIP runtime refused a launch */
+} rf_status;
+
+/* Element types; passed as int32_t. */
+typedef enum { RF_BF16 = 0, RF_F32 = 1 } rf_dtype;
+
+/* Flags of rf_select_keyframes. */
+#define RF_SEL_NO_FORCE_FIRST 1u
+
+/* Name of a status code (static string). */
+const char *rf_status_string(int status);
+/* Description of the last failure on this thread ("" if none). */
+const char *rf_last_error(void);
+/* RF_ABI_VERSION of the loaded library. */
+int rf_abi_version(void);
+
+/*
+ * Keyframe set from an explicit frame list (host only, integer, bit-exact).
+ *
+ * The keyframe set K is a set of frame indices; the first frame always belongs
+ * to it, as the anchor of the video (Sec. 3.1; Alg. 1 starts K with the first
+ * frame). Non-keyframes are the complement (Alg. 1).
+ *
+ * frame_ids [n_ids]: any order, duplicates allowed, each in [0, T).
+ * T: frames, 1..RF_MAX_FRAMES.
+ * flags: RF_SEL_NO_FORCE_FIRST leaves frame 0 out unless listed.
+ * keyframe_ids_out [T capacity]: K sorted ascending, no duplicates.
+ * num_keyframes_out: |K|.
+ * keyframe_mask_out [T] (may be NULL): 1 for keyframes, 0 otherwise.
+ * Errors: RF_ERR_INVALID_ARG (NULL outputs, n_ids < 0, frame_ids NULL with
+ * n_ids > 0, empty result), RF_ERR_RANGE (an id outside [0, T) or T outside
+ * 1..RF_MAX_FRAMES). Outputs are written only on success.
+ */
+int rf_select_keyframes(const int32_t *frame_ids, int32_t n_ids, int32_t T,
+                        uint32_t flags, int32_t *keyframe_ids_out,
+                        int32_t *num_keyframes_out, uint8_t *keyframe_mask_out);
+
+/* Fixed-interval policy: frames 0, k, 2k, ... below T. ids_out has capacity T.
+   Errors: RF_ERR_INVALID_ARG (NULL, k <= 0), RF_ERR_RANGE (T outside 1..RF_MAX_FRAMES). */
+int rf_keyframes_stride(int32_t T, int32_t k, int32_t *ids_out, int32_t *n_out);
+
+/* Evenly spaced policy ("Uniform" in the selection ablation, Sec. 4): M frames
+   i*(T-1)/(M-1) rounded half up, i = 0..M-1, first and last included; M = 1
+   gives frame 0. ids_out has capacity M.
+   Errors: RF_ERR_INVALID_ARG (NULL), RF_ERR_RANGE (M outside 1..T, T outside
+   1..RF_MAX_FRAMES). */
+int rf_keyframes_uniform(int32_t T, int32_t M, int32_t *ids_out, int32_t *n_out);
+
+/*
+ * Latent trajectory projection, Eq. (3) (Sec. 3.2.4):
+ *   z_hat(tau) = (1 - alpha) z(t_start) + alpha z(t_end),
+ *   alpha = (t_start - tau) / (t_start - t_end),
+ * for the non-keyframes; keyframes keep their current (true) state.
+ *
+ * latents: device [B][2][C][T][Hl][Wl], contiguous. Slot 0 holds z(t_start);
+ *          slot 1 holds z(t_end) for non-keyframes and the current state for
+ *          keyframes.
+ * out:     device [B][C][T][Hl][Wl], contiguous. It may be exactly slot 1 of a
+ *          single batch (B == 1, out == latents + C*T*Hl*Wl elements): keyframe
+ *          planes are then left untouched. Any other overlap is an error.
+ * timesteps: host {t_start, t_end, tau}, finite doubles (step indices or
+ *          scheduler times; only their ratios matter). alpha is computed in
+ *          double, kept inside [0, 1], and is 1 when t_start == t_end; it is
+ *          then rounded once to float. Each element is evaluated as
+ *          fmaf(alpha, z_end, (1 - alpha) * z_start) in fp32, so alpha = 0
+ *          returns z_start and alpha = 1 returns z_end exactly.
+ * keyframe_mask: host [T] bytes, nonzero = keyframe.
+ * dtype:   RF_F32 or RF_BF16 storage for latents and out (fp32 arithmetic;
+ *          bf16 results rounded to nearest even).
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0, non-finite timesteps, partial
+ *         overlap of out and latents), RF_ERR_RANGE (T > RF_MAX_FRAMES),
+ *         RF_ERR_UNSUPPORTED (unknown dtype, misaligned pointer), RF_ERR_HIP.
+ */
+int rf_project_latents(const void *latents, void *out, const double timesteps[3],
+                       const uint8_t *keyframe_mask, int32_t B, int32_t C,
+                       int32_t T, int32_t Hl, int32_t Wl, int32_t dtype,
+                       void *stream);
+
+/*
+ * Keyframe-query attention (Sec. 3.2.3-3.2.4; App. B.2, attention at skipped
+ * steps): the query rows are the N = H*W tokens of each keyframe; keys and
+ * values are all S = T*N tokens of all frames. Per head,
+ *   out = softmax(Q_kf K^T / sqrt(head_dim)) V,
+ * with no mask. The query gather is fused: non-keyframe rows of q are never read.
+ *
+ * q, k, v: device [S][heads][head_dim], contiguous, token index
+ *          f*N + y*W + x for frame f, row y, column x.
+ * out:     device [M*N][heads][head_dim], contiguous; row r holds the query
+ *          token keyframe_ids[r / N]*N + r % N (keyframe order). Must not
+ *          overlap q, k or v.
+ * keyframe_ids: host [M], strictly increasing, each in [0, T).
+ * M = T with ids 0..T-1 is full 3D attention over all frames (warm-up steps
+ * and Rhythmic Points, Sec. 3.2.1, 3.2.3).
+ * head_dim: 64 or 128. dtype: RF_BF16 (bf16 inputs and output, bf16 matrix
+ *          cores, fp32 softmax and accumulation, output rounded to nearest
+ *          even) or RF_F32 (fp32 throughout, a correctness path).
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0, ids not strictly increasing,
+ *         out overlapping an input), RF_ERR_RANGE (an id outside [0, T), M > T,
+ *         T > RF_MAX_FRAMES), RF_ERR_UNSUPPORTED (head_dim, dtype, alignment),
+ *         RF_ERR_HIP.
+ */
+int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out,
+                          const int32_t *keyframe_ids, int32_t M, int32_t T,
+                          int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                          int32_t dtype, void *stream);
+
+/*
+ * Frame gather: dst_compact[m*N + n] = src_full[frame_ids[m]*N + n] for rows
+ * of row_bytes bytes, N = rows_per_frame; every frame is one contiguous block
+ * of N rows (the token layout of a frame-major sequence, App. B.1: S = F x N).
+ * A bit-exact copy; standalone form of the query gather fused into
+ * rf_keyframe_attention.
+ *
+ * src_full: device, T*N rows. dst_compact: device, M*N rows; no overlap.
+ * frame_ids: host [M], strictly increasing, each in [0, T).
+ * row_bytes: a multiple of 16.
+ * Errors: RF_ERR_INVALID_ARG, RF_ERR_RANGE, RF_ERR_UNSUPPORTED (alignment,
+ *         row_bytes % 16), RF_ERR_HIP.
+ */
+int rf_gather_frames(const void *src_full, void *dst_compact,
+                     const int32_t *frame_ids, int32_t M, int32_t T,
+                     int64_t rows_per_frame, int64_t row_bytes, void *stream);
+
+/*
+ * Frame scatter, the inverse of rf_gather_frames: writes the keyframe rows of
+ * a compact attention output back to their token positions,
+ * dst_full[frame_ids[m]*N + n] = src_compact[m*N + n]. Rows of frames not
+ * listed are left untouched (their outputs come from elsewhere, App. B.2).
+ * Same arguments and errors as rf_gather_frames.
+ */
+int rf_scatter_frames(const void *src_compact, void *dst_full,
+                      const int32_t *frame_ids, int32_t M, int32_t T,
+                      int64_t rows_per_frame, int64_t row_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RHYMEFLOW_H */

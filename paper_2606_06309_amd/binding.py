@@ -1,0 +1,226 @@
+"""Thin Python binding over librhymeflow.so (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of the method: it checks that tensors are contiguous device tensors
+of the right dtype, passes their device pointers and torch's current HIP
+stream, and turns a nonzero status into RhymeFlowError. All compute runs in
+the HIP kernels; there is no CPU fallback. Importing this module fails loudly
+if the library has not been built.
+"""
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librhymeflow.so")
+
+RF_OK = 0
+RF_ERR_INVALID_ARG = -1
+RF_ERR_UNSUPPORTED = -2
+RF_ERR_RANGE = -3
+RF_ERR_HIP = -4
+RF_BF16 = 0
+RF_F32 = 1
+RF_SEL_NO_FORCE_FIRST = 1
+RF_MAX_FRAMES = 256
+
+EXPORTED = [
+    "rf_status_string", "rf_last_error", "rf_abi_version",
+    "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
+    "rf_project_latents", "rf_keyframe_attention",
+    "rf_gather_frames", "rf_scatter_frames",
+]
+
+
+class RhymeFlowError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} [{status}]")
+        self.status = status
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build the HIP library first "
+        "(python -c 'import __graft_entry__ as g; g.build()')")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+_dp = ctypes.POINTER(ctypes.c_double)
+
+lib.rf_status_string.argtypes = [ctypes.c_int]
+lib.rf_status_string.restype = ctypes.c_char_p
+lib.rf_last_error.argtypes = []
+lib.rf_last_error.restype = ctypes.c_char_p
+lib.rf_abi_version.argtypes = []
+lib.rf_abi_version.restype = ctypes.c_int
+lib.rf_select_keyframes.argtypes = [_i32p, _i32, _i32, ctypes.c_uint32, _i32p, _i32p, _u8p]
+lib.rf_select_keyframes.restype = ctypes.c_int
+lib.rf_keyframes_stride.argtypes = [_i32, _i32, _i32p, _i32p]
+lib.rf_keyframes_stride.restype = ctypes.c_int
+lib.rf_keyframes_uniform.argtypes = [_i32, _i32, _i32p, _i32p]
+lib.rf_keyframes_uniform.restype = ctypes.c_int
+lib.rf_project_latents.argtypes = [_vp, _vp, _dp, _u8p, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
+lib.rf_project_latents.restype = ctypes.c_int
+lib.rf_keyframe_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
+                                      _i32, _i32, _i32, _vp]
+lib.rf_keyframe_attention.restype = ctypes.c_int
+lib.rf_gather_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
+lib.rf_gather_frames.restype = ctypes.c_int
+lib.rf_scatter_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
+lib.rf_scatter_frames.restype = ctypes.c_int
+
+
+def _check(status: int):
+    if status != RF_OK:
+        msg = lib.rf_last_error().decode(errors="replace")
+        raise RhymeFlowError(status, f"{lib.rf_status_string(status).decode()}: {msg}")
+
+
+def _ids(ids):
+    a = np.ascontiguousarray(np.asarray(list(ids), dtype=np.int32))
+    return a, a.ctypes.data_as(_i32p)
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(dt):
+    if dt == torch.bfloat16:
+        return RF_BF16
+    if dt == torch.float32:
+        return RF_F32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def abi_version() -> int:
+    return int(lib.rf_abi_version())
+
+
+# --- keyframe sets (host) ------------------------------------------------------
+
+def rf_select_keyframes(frame_ids, T: int, force_first: bool = True):
+    """Returns (keyframe ids int32 [M], mask uint8 [T])."""
+    ids, ids_p = _ids(frame_ids)
+    out = np.zeros(max(T, 1), dtype=np.int32)
+    mask = np.zeros(max(T, 1), dtype=np.uint8)
+    n = ctypes.c_int32(0)
+    flags = 0 if force_first else RF_SEL_NO_FORCE_FIRST
+    _check(lib.rf_select_keyframes(ids_p if ids.size else None, ids.size, T, flags,
+                                   out.ctypes.data_as(_i32p), ctypes.byref(n),
+                                   mask.ctypes.data_as(_u8p)))
+    return out[:n.value].copy(), mask[:T].copy()
+
+
+def rf_keyframes_stride(T: int, k: int) -> np.ndarray:
+    out = np.zeros(max(T, 1), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib.rf_keyframes_stride(T, k, out.ctypes.data_as(_i32p), ctypes.byref(n)))
+    return out[:n.value].copy()
+
+
+def rf_keyframes_uniform(T: int, M: int) -> np.ndarray:
+    out = np.zeros(max(M, 1), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib.rf_keyframes_uniform(T, M, out.ctypes.data_as(_i32p), ctypes.byref(n)))
+    return out[:n.value].copy()
+
+
+# --- device calls ----------------------------------------------------------------
+
+def rf_project_latents(latents: torch.Tensor, timesteps, keyframe_mask, out=None, stream=None):
+    """latents [B][2][C][T][Hl][Wl] -> out [B][C][T][Hl][Wl] (same dtype)."""
+    if latents.dim() != 6 or latents.shape[1] != 2:
+        raise ValueError("latents must be [B][2][C][T][Hl][Wl]")
+    B, _, C, T, Hl, Wl = latents.shape
+    if out is None:
+        out = torch.empty((B, C, T, Hl, Wl), dtype=latents.dtype, device=latents.device)
+    if out.dtype != latents.dtype or out.numel() != B * C * T * Hl * Wl:
+        raise ValueError("out must match latents' dtype and [B][C][T][Hl][Wl] size")
+    ts = (ctypes.c_double * 3)(*[float(x) for x in timesteps])
+    mask = np.ascontiguousarray(np.asarray(keyframe_mask, dtype=np.uint8))
+    if mask.size != T:
+        raise ValueError("keyframe_mask must have T entries")
+    _check(lib.rf_project_latents(_dev(latents, "latents"), _dev(out, "out"), ts,
+                                  mask.ctypes.data_as(_u8p), B, C, T, Hl, Wl,
+                                  _dtype_code(latents.dtype), _stream(stream)))
+    return out
+
+
+def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=None, stream=None):
+    """q, k, v [T*H*W][heads][head_dim] -> out [M*H*W][heads][head_dim]."""
+    if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share a dtype")
+    S, heads, d = q.shape
+    if S != T * H * W:
+        raise ValueError(f"S = {S} differs from T*H*W = {T * H * W}")
+    ids, ids_p = _ids(keyframe_ids)
+    M = ids.size
+    if out is None:
+        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+    if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
+        raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
+    _check(lib.rf_keyframe_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                     ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
+                                     _stream(stream)))
+    return out
+
+
+def _row_geometry(t: torch.Tensor, rows_per_frame: int):
+    if t.dim() < 1 or t.shape[0] % rows_per_frame:
+        raise ValueError("leading dimension must be a multiple of rows_per_frame")
+    return t.numel() // t.shape[0] * t.element_size()
+
+
+def rf_gather_frames(src_full: torch.Tensor, frame_ids, T: int, rows_per_frame: int,
+                     out=None, stream=None):
+    """src_full [T*N][...] -> out [M*N][...] (rows of the listed frames)."""
+    row_bytes = _row_geometry(src_full, rows_per_frame)
+    if src_full.shape[0] != T * rows_per_frame:
+        raise ValueError("src_full must hold T * rows_per_frame rows")
+    ids, ids_p = _ids(frame_ids)
+    if out is None:
+        out = torch.empty((ids.size * rows_per_frame,) + tuple(src_full.shape[1:]),
+                          dtype=src_full.dtype, device=src_full.device)
+    if out.numel() * out.element_size() != ids.size * rows_per_frame * row_bytes:
+        raise ValueError("out must hold M * rows_per_frame rows")
+    _check(lib.rf_gather_frames(_dev(src_full, "src_full"), _dev(out, "out"), ids_p, ids.size, T,
+                                rows_per_frame, row_bytes, _stream(stream)))
+    return out
+
+
+def rf_scatter_frames(src_compact: torch.Tensor, dst_full: torch.Tensor, frame_ids, T: int,
+                      rows_per_frame: int, stream=None):
+    """Writes src_compact's rows into the listed frames of dst_full (in place)."""
+    row_bytes = _row_geometry(dst_full, rows_per_frame)
+    if dst_full.shape[0] != T * rows_per_frame:
+        raise ValueError("dst_full must hold T * rows_per_frame rows")
+    ids, ids_p = _ids(frame_ids)
+    if src_compact.numel() * src_compact.element_size() != ids.size * rows_per_frame * row_bytes:
+        raise ValueError("src_compact must hold M * rows_per_frame rows of dst_full's row size")
+    _check(lib.rf_scatter_frames(_dev(src_compact, "src_compact"), _dev(dst_full, "dst_full"),
+                                 ids_p, ids.size, T, rows_per_frame, row_bytes, _stream(stream)))
+    return dst_full

@@ -1,0 +1,272 @@
+// C ABI of librhymeflow.so: argument validation, kernel-argument packing and
+// launch on the caller's stream. Every check runs before the first HIP call.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "rf_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return RF_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Half-open byte ranges [a, a+na) and [b, b+nb) intersect.
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
+    const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + static_cast<uintptr_t>(nb) && pb < pa + static_cast<uintptr_t>(na);
+}
+
+int launched(hipError_t e, const char *what) {
+    if (e != hipSuccess)
+        return fail(RF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+// Strictly increasing ids in [0, T), copied into dst.
+int check_id_list(const int32_t *ids, int32_t M, int32_t T, int32_t *dst, const char *what) {
+    if (!ids) return fail(RF_ERR_INVALID_ARG, "%s: id list is NULL", what);
+    if (M <= 0) return fail(RF_ERR_INVALID_ARG, "%s: M = %d must be positive", what, M);
+    if (T <= 0) return fail(RF_ERR_INVALID_ARG, "%s: T = %d must be positive", what, T);
+    if (T > RF_MAX_FRAMES)
+        return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d frames", what, T, RF_MAX_FRAMES);
+    if (M > T) return fail(RF_ERR_RANGE, "%s: M = %d exceeds T = %d", what, M, T);
+    for (int32_t i = 0; i < M; ++i) {
+        if (ids[i] < 0 || ids[i] >= T)
+            return fail(RF_ERR_RANGE, "%s: id %d at position %d outside [0, %d)", what, ids[i], i, T);
+        if (i > 0 && ids[i] <= ids[i - 1])
+            return fail(RF_ERR_INVALID_ARG, "%s: ids not strictly increasing at position %d", what, i);
+        dst[i] = ids[i];
+    }
+    return RF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *rf_status_string(int status) {
+    switch (status) {
+        case RF_OK: return "RF_OK";
+        case RF_ERR_INVALID_ARG: return "RF_ERR_INVALID_ARG";
+        case RF_ERR_UNSUPPORTED: return "RF_ERR_UNSUPPORTED";
+        case RF_ERR_RANGE: return "RF_ERR_RANGE";
+        case RF_ERR_HIP: return "RF_ERR_HIP";
+        default: return "RF_UNKNOWN_STATUS";
+    }
+}
+
+const char *rf_last_error(void) { return g_err; }
+
+int rf_abi_version(void) { return RF_ABI_VERSION; }
+
+int rf_select_keyframes(const int32_t *frame_ids, int32_t n_ids, int32_t T, uint32_t flags,
+                        int32_t *keyframe_ids_out, int32_t *num_keyframes_out,
+                        uint8_t *keyframe_mask_out) {
+    if (!keyframe_ids_out || !num_keyframes_out)
+        return fail(RF_ERR_INVALID_ARG, "rf_select_keyframes: NULL output");
+    if (n_ids < 0) return fail(RF_ERR_INVALID_ARG, "rf_select_keyframes: n_ids < 0");
+    if (n_ids > 0 && !frame_ids)
+        return fail(RF_ERR_INVALID_ARG, "rf_select_keyframes: frame_ids is NULL");
+    if (T <= 0 || T > RF_MAX_FRAMES)
+        return fail(RF_ERR_RANGE, "rf_select_keyframes: T = %d outside 1..%d", T, RF_MAX_FRAMES);
+    if (flags & ~RF_SEL_NO_FORCE_FIRST)
+        return fail(RF_ERR_INVALID_ARG, "rf_select_keyframes: unknown flags 0x%x", flags);
+    uint8_t member[RF_MAX_FRAMES] = {0};
+    for (int32_t i = 0; i < n_ids; ++i) {
+        if (frame_ids[i] < 0 || frame_ids[i] >= T)
+            return fail(RF_ERR_RANGE, "rf_select_keyframes: id %d outside [0, %d)", frame_ids[i], T);
+        member[frame_ids[i]] = 1;
+    }
+    if (!(flags & RF_SEL_NO_FORCE_FIRST)) member[0] = 1;  // the first frame anchors the video
+    int32_t n = 0;
+    for (int32_t f = 0; f < T; ++f) n += member[f];
+    if (n == 0) return fail(RF_ERR_INVALID_ARG, "rf_select_keyframes: empty keyframe set");
+    n = 0;
+    for (int32_t f = 0; f < T; ++f)
+        if (member[f]) keyframe_ids_out[n++] = f;
+    *num_keyframes_out = n;
+    if (keyframe_mask_out)
+        for (int32_t f = 0; f < T; ++f) keyframe_mask_out[f] = member[f];
+    return ok();
+}
+
+int rf_keyframes_stride(int32_t T, int32_t k, int32_t *ids_out, int32_t *n_out) {
+    if (!ids_out || !n_out) return fail(RF_ERR_INVALID_ARG, "rf_keyframes_stride: NULL output");
+    if (k <= 0) return fail(RF_ERR_INVALID_ARG, "rf_keyframes_stride: k = %d must be positive", k);
+    if (T <= 0 || T > RF_MAX_FRAMES)
+        return fail(RF_ERR_RANGE, "rf_keyframes_stride: T = %d outside 1..%d", T, RF_MAX_FRAMES);
+    int32_t n = 0;
+    for (int32_t f = 0; f < T; f += k) ids_out[n++] = f;
+    *n_out = n;
+    return ok();
+}
+
+int rf_keyframes_uniform(int32_t T, int32_t M, int32_t *ids_out, int32_t *n_out) {
+    if (!ids_out || !n_out) return fail(RF_ERR_INVALID_ARG, "rf_keyframes_uniform: NULL output");
+    if (T <= 0 || T > RF_MAX_FRAMES)
+        return fail(RF_ERR_RANGE, "rf_keyframes_uniform: T = %d outside 1..%d", T, RF_MAX_FRAMES);
+    if (M <= 0 || M > T)
+        return fail(RF_ERR_RANGE, "rf_keyframes_uniform: M = %d outside 1..%d", M, T);
+    if (M == 1) {
+        ids_out[0] = 0;
+        *n_out = 1;
+        return ok();
+    }
+    // nearest integer to i*(T-1)/(M-1), halves rounded up: floor((2i(T-1) + (M-1)) / (2(M-1)))
+    for (int32_t i = 0; i < M; ++i) {
+        const int64_t num = 2LL * i * (T - 1) + (M - 1);
+        ids_out[i] = static_cast<int32_t>(num / (2LL * (M - 1)));
+    }
+    *n_out = M;
+    return ok();
+}
+
+int rf_project_latents(const void *latents, void *out, const double timesteps[3],
+                       const uint8_t *keyframe_mask, int32_t B, int32_t C, int32_t T,
+                       int32_t Hl, int32_t Wl, int32_t dtype, void *stream) {
+    const char *fn = "rf_project_latents";
+    if (!latents || !out || !timesteps || !keyframe_mask)
+        return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);
+    if (B <= 0 || C <= 0 || T <= 0 || Hl <= 0 || Wl <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (B=%d C=%d T=%d Hl=%d Wl=%d)",
+                    fn, B, C, T, Hl, Wl);
+    if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
+    if (dtype != RF_F32 && dtype != RF_BF16)
+        return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    const double t_start = timesteps[0], t_end = timesteps[1], tau = timesteps[2];
+    if (!isfinite(t_start) || !isfinite(t_end) || !isfinite(tau))
+        return fail(RF_ERR_INVALID_ARG, "%s: timesteps must be finite", fn);
+    if (!aligned16(latents) || !aligned16(out))
+        return fail(RF_ERR_UNSUPPORTED, "%s: pointers must be 16-byte aligned", fn);
+
+    const int64_t elem = dtype == RF_F32 ? 4 : 2;
+    const int64_t plane = static_cast<int64_t>(Hl) * Wl;
+    const int64_t slot_bytes = static_cast<int64_t>(C) * T * plane * elem;
+    const int64_t lat_bytes = static_cast<int64_t>(B) * 2 * slot_bytes;
+    const int64_t out_bytes = static_cast<int64_t>(B) * slot_bytes;
+    const char *slot1 = static_cast<const char *>(latents) + slot_bytes;
+    int skip_keyframes = 0;
+    if (B == 1 && out == slot1) {
+        skip_keyframes = 1;  // out is slot 1 itself: keyframe planes already hold their state
+    } else if (overlaps(latents, lat_bytes, out, out_bytes)) {
+        return fail(RF_ERR_INVALID_ARG, "%s: out overlaps latents (only out == slot 1 with B == 1 is allowed)", fn);
+    }
+
+    rf::ProjParams p{};
+    p.latents = latents;
+    p.out = out;
+    p.plane = plane;
+    p.B = B;
+    p.C = C;
+    p.T = T;
+    p.dtype = dtype;
+    p.skip_keyframes = skip_keyframes;
+    // Eq. (3): alpha = (t_start - tau) / (t_start - t_end), in double, kept in
+    // [0, 1]; equal endpoints (both snapshots the same state) give 1.
+    double alpha = 1.0;
+    if (t_start != t_end) {
+        alpha = (t_start - tau) / (t_start - t_end);
+        alpha = alpha < 0.0 ? 0.0 : (alpha > 1.0 ? 1.0 : alpha);
+    }
+    p.alpha = static_cast<float>(alpha);
+    for (int32_t f = 0; f < T; ++f) p.is_key[f] = keyframe_mask[f] ? 1 : 0;
+    return launched(rf::launch_projection(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out,
+                          const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H,
+                          int32_t W, int32_t heads, int32_t head_dim, int32_t dtype,
+                          void *stream) {
+    const char *fn = "rf_keyframe_attention";
+    if (!q || !k || !v || !out) return fail(RF_ERR_INVALID_ARG, "%s: NULL tensor", fn);
+    if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
+                    fn, H, W, heads, head_dim);
+    rf::AttnParams p{};
+    const int rc = check_id_list(keyframe_ids, M, T, p.kf, fn);
+    if (rc != RF_OK) return rc;
+    if (head_dim != 64 && head_dim != 128)
+        return fail(RF_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
+    if (dtype != RF_BF16 && dtype != RF_F32)
+        return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+        return fail(RF_ERR_UNSUPPORTED, "%s: pointers must be 16-byte aligned", fn);
+
+    const int64_t N = static_cast<int64_t>(H) * W;
+    const int64_t S = N * T;
+    const int64_t row = static_cast<int64_t>(heads) * head_dim * (dtype == RF_F32 ? 4 : 2);
+    const int64_t in_bytes = S * row;
+    const int64_t out_bytes = N * M * row;
+    if (overlaps(out, out_bytes, q, in_bytes) || overlaps(out, out_bytes, k, in_bytes) ||
+        overlaps(out, out_bytes, v, in_bytes))
+        return fail(RF_ERR_INVALID_ARG, "%s: out overlaps q, k or v", fn);
+
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.out = out;
+    p.S = S;
+    p.N = N;
+    p.M = M;
+    p.heads = heads;
+    p.head_dim = head_dim;
+    p.dtype = dtype;
+    return launched(rf::launch_attention(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int32_t M, int32_t T,
+                      int64_t rows_per_frame, int64_t row_bytes, void *stream, int scatter,
+                      const char *fn) {
+    if (!src || !dst) return fail(RF_ERR_INVALID_ARG, "%s: NULL buffer", fn);
+    if (rows_per_frame <= 0 || row_bytes <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: rows_per_frame and row_bytes must be positive", fn);
+    rf::FrameCopyParams p{};
+    const int rc = check_id_list(frame_ids, M, T, p.ids, fn);
+    if (rc != RF_OK) return rc;
+    if (row_bytes % 16 != 0)
+        return fail(RF_ERR_UNSUPPORTED, "%s: row_bytes %lld not a multiple of 16", fn,
+                    static_cast<long long>(row_bytes));
+    if (!aligned16(src) || !aligned16(dst))
+        return fail(RF_ERR_UNSUPPORTED, "%s: pointers must be 16-byte aligned", fn);
+    const int64_t frame_bytes = rows_per_frame * row_bytes;
+    const int64_t full = frame_bytes * T, compact = frame_bytes * M;
+    if (overlaps(src, scatter ? compact : full, dst, scatter ? full : compact))
+        return fail(RF_ERR_INVALID_ARG, "%s: source and destination overlap", fn);
+    p.src = src;
+    p.dst = dst;
+    p.frame_bytes = frame_bytes;
+    p.M = M;
+    p.scatter = scatter;
+    return launched(rf::launch_frame_copy(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_gather_frames(const void *src_full, void *dst_compact, const int32_t *frame_ids, int32_t M,
+                     int32_t T, int64_t rows_per_frame, int64_t row_bytes, void *stream) {
+    return frame_copy(src_full, dst_compact, frame_ids, M, T, rows_per_frame, row_bytes, stream, 0,
+                      "rf_gather_frames");
+}
+
+int rf_scatter_frames(const void *src_compact, void *dst_full, const int32_t *frame_ids, int32_t M,
+                      int32_t T, int64_t rows_per_frame, int64_t row_bytes, void *stream) {
+    return frame_copy(src_compact, dst_full, frame_ids, M, T, rows_per_frame, row_bytes, stream, 1,
+                      "rf_scatter_frames");
+}
+
+}  // extern "C"

@@ -1,0 +1,390 @@
+// Keyframe-query attention for gfx950 (CDNA4).
+//
+// Method (Sec. 3.2.3-3.2.4; App. B.2): at a step where only keyframes are
+// denoised, the query tokens of the M keyframes attend over the keys and
+// values of all T frames. Per head: out = softmax(Q_kf K^T / sqrt(d)) V.
+//
+// bf16 kernel design:
+//  * A workgroup of 4 waves owns one (head, 128-row query tile); each wave
+//    owns 32 query rows. Query rows are gathered straight from the keyframe
+//    tokens (row r reads token kf[r / N] * N + r % N), so the gather is fused
+//    and non-keyframe query rows are never read.
+//  * Scores are computed transposed, S^T = K Q^T, with
+//    v_mfma_f32_32x32x16_bf16: K rows are the A operand (from LDS), the
+//    wave's query rows the B operand (held in registers for the whole loop).
+//    In the 32x32 accumulator layout every lane then holds 16 scores of ONE
+//    query column, so the softmax max and sum are in-lane reductions plus one
+//    exchange with the lane 32 apart.
+//  * The probabilities are already in the B-operand layout of the second
+//    product, O^T = V^T P^T: the lane's 16 accumulators become two bf16x8
+//    operands without any data movement. V is staged transposed in LDS
+//    ([d][key]) so each A operand is two 64-bit LDS reads; the key order
+//    inside an operand follows the accumulator layout (a reduction index may
+//    be permuted freely as long as both operands agree).
+//  * Online softmax in the log2 domain with fp32 state; P is rounded to bf16
+//    for the matrix cores, the row sum uses the unrounded fp32 values.
+//  * K/V tiles of 64 keys are prefetched into registers while the current
+//    tile is computed; the last tile masks keys >= S.
+//  * Workgroup ids are mapped XCD-aware: consecutive ids go round-robin to the
+//    8 XCDs, so tile = (id % 8) * per_xcd + id / 8 gives each XCD a contiguous,
+//    head-major range of tiles and the workgroups resident on one XCD stream
+//    the same head's K/V through that XCD's L2.
+#include "rf_internal.h"
+
+namespace rf {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBr = 32 * kWaves;   // query rows per workgroup
+constexpr int kBc = 64;            // keys per tile
+constexpr int kKPad = 8;           // bf16 padding per K row in LDS (row = 272 B at d=128)
+constexpr int kVPad = 4;           // bf16 padding per V^T row in LDS (row = 136 B)
+constexpr int kXcds = 8;
+
+struct AttnKArgs {
+    const __bf16 *q;
+    const __bf16 *k;
+    const __bf16 *v;
+    __bf16 *out;
+    int64_t S;
+    int64_t N;
+    int64_t Mq;
+    int32_t heads;
+    int32_t n_qtiles;
+    int32_t total_tiles;
+    int32_t per_xcd;
+    float scale_log2;   // log2(e) / sqrt(d)
+    int32_t kf[kMaxFrames];
+};
+
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) {
+    constexpr int kKRow = D + kKPad;
+    constexpr int kVRow = kBc + kVPad;
+    constexpr int kKChunks = kBc * D / 8 / kThreads;    // 16-byte K chunks per thread
+    constexpr int kVChunks = kBc * D / 16 / kThreads;   // (2 keys x 8 dims) V chunks per thread
+    static_assert(kKChunks >= 1 && kVChunks >= 1, "tile too small for the workgroup");
+
+    __shared__ __attribute__((aligned(16))) __bf16 ks[kBc * kKRow];
+    __shared__ __attribute__((aligned(16))) __bf16 vt[D * kVRow];
+
+    const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
+    if (tile >= a.total_tiles) return;
+    const int head = tile / a.n_qtiles;
+    const int qt = tile - head * a.n_qtiles;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 31, grp = lane >> 5;
+    const int64_t rs = static_cast<int64_t>(a.heads) * D;   // token stride in elements
+
+    // ---- query fragments: B operand of S^T = K Q^T (fused keyframe gather) ----
+    const int64_t row = static_cast<int64_t>(qt) * kBr + wave * 32 + col;
+    bf16x8_t qf[D / 16];
+    if (row < a.Mq) {
+        const int64_t f = row / a.N;
+        const int64_t tok = static_cast<int64_t>(a.kf[f]) * a.N + (row - f * a.N);
+        const __bf16 *qp = a.q + tok * rs + static_cast<int64_t>(head) * D + grp * 8;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t *>(qp + kk * 16);
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qf[kk][e] = static_cast<__bf16>(0.0f);
+    }
+
+    f32x16_t oacc[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
+    float m_run = -__builtin_huge_valf();   // running max, log2 domain
+    float l_run = 0.0f;                     // this lane's partial row sum
+
+    const __bf16 *kbase = a.k + static_cast<int64_t>(head) * D;
+    const __bf16 *vbase = a.v + static_cast<int64_t>(head) * D;
+
+    bf16x8_t kreg[kKChunks], vreg0[kVChunks], vreg1[kVChunks];
+    bf16x8_t zero8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) zero8[e] = static_cast<__bf16>(0.0f);
+
+    auto load_tile = [&](int64_t j0) {
+#pragma unroll
+        for (int i = 0; i < kKChunks; ++i) {
+            const int c = tid + i * kThreads;
+            const int key = c / (D / 8), c8 = c % (D / 8);
+            const int64_t j = j0 + key;
+            kreg[i] = j < a.S ? *reinterpret_cast<const bf16x8_t *>(kbase + j * rs + c8 * 8) : zero8;
+        }
+#pragma unroll
+        for (int i = 0; i < kVChunks; ++i) {
+            const int p = tid + i * kThreads;
+            const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
+            const int64_t j = j0 + 2 * kp;
+            vreg0[i] = j < a.S ? *reinterpret_cast<const bf16x8_t *>(vbase + j * rs + c8 * 8) : zero8;
+            vreg1[i] = j + 1 < a.S ? *reinterpret_cast<const bf16x8_t *>(vbase + (j + 1) * rs + c8 * 8) : zero8;
+        }
+    };
+    auto store_tile = [&]() {
+#pragma unroll
+        for (int i = 0; i < kKChunks; ++i) {
+            const int c = tid + i * kThreads;
+            const int key = c / (D / 8), c8 = c % (D / 8);
+            *reinterpret_cast<bf16x8_t *>(&ks[key * kKRow + c8 * 8]) = kreg[i];
+        }
+#pragma unroll
+        for (int i = 0; i < kVChunks; ++i) {
+            const int p = tid + i * kThreads;
+            const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                // keys 2kp and 2kp+1 of dimension c8*8+e, adjacent in the transposed row
+                const uint32_t lo = __builtin_bit_cast(uint16_t, vreg0[i][e]);
+                const uint32_t hi = __builtin_bit_cast(uint16_t, vreg1[i][e]);
+                *reinterpret_cast<uint32_t *>(&vt[(c8 * 8 + e) * kVRow + 2 * kp]) = lo | (hi << 16);
+            }
+        }
+    };
+
+    const int64_t ntiles = (a.S + kBc - 1) / kBc;
+    const float sl2 = a.scale_log2;
+    load_tile(0);
+    for (int64_t t = 0; t < ntiles; ++t) {
+        __syncthreads();   // every wave is done reading the previous tile
+        store_tile();
+        __syncthreads();
+        if (t + 1 < ntiles) load_tile((t + 1) * kBc);   // in flight during this tile's math
+
+        // ---- S^T = K Q^T : two 32-key blocks ----
+        f32x16_t sacc[kBc / 32];
+#pragma unroll
+        for (int b = 0; b < kBc / 32; ++b) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sacc[b][r] = 0.0f;
+#pragma unroll
+            for (int kk = 0; kk < D / 16; ++kk) {
+                const bf16x8_t kfrag =
+                    *reinterpret_cast<const bf16x8_t *>(&ks[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
+                sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag, qf[kk], sacc[b], 0, 0, 0);
+            }
+        }
+        // accumulator r of block b holds key b*32 + (r/4)*8 + grp*4 + r%4 for query `col`
+
+        const int64_t j0 = t * kBc;
+        if (j0 + kBc > a.S) {
+#pragma unroll
+            for (int b = 0; b < kBc / 32; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t key = j0 + b * 32 + (r / 4) * 8 + grp * 4 + (r % 4);
+                    if (key >= a.S) sacc[b][r] = -__builtin_huge_valf();
+                }
+        }
+
+        // ---- online softmax (log2 domain) ----
+        float mx = -__builtin_huge_valf();
+#pragma unroll
+        for (int b = 0; b < kBc / 32; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[b][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx * sl2);
+        const float corr = fast_exp2(m_run - m_new);
+        m_run = m_new;
+
+        bf16x8_t pb[kBc / 16];
+        float ls = 0.0f;
+#pragma unroll
+        for (int b = 0; b < kBc / 32; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = fast_exp2(fmaf(sacc[b][r], sl2, -m_new));
+                ls += p;
+                pb[b * 2 + r / 8][r % 8] = static_cast<__bf16>(p);
+            }
+        l_run = fmaf(l_run, corr, ls);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[db][r] *= corr;
+
+        // ---- O^T += V^T P^T ----
+#pragma unroll
+        for (int c = 0; c < kBc / 16; ++c) {
+            const int key0 = (c / 2) * 32 + (c % 2) * 16 + grp * 4;   // operand elements 0..3
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) {
+                const __bf16 *vrow = &vt[(db * 32 + col) * kVRow];
+                const bf16x4_t lo = *reinterpret_cast<const bf16x4_t *>(vrow + key0);
+                const bf16x4_t hi = *reinterpret_cast<const bf16x4_t *>(vrow + key0 + 8);
+                const bf16x8_t vfrag = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag, pb[c], oacc[db], 0, 0, 0);
+            }
+        }
+    }
+
+    // ---- epilogue: normalise, round to bf16, store the compact row ----
+    l_run += __shfl_xor(l_run, 32);
+    if (row < a.Mq) {
+        const float inv = 1.0f / l_run;
+        __bf16 *op = a.out + row * rs + static_cast<int64_t>(head) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                // accumulator r holds dimension db*32 + (r/4)*8 + grp*4 + r%4
+                bf16x4_t o4;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o4[e] = static_cast<__bf16>(oacc[db][g4 * 4 + e] * inv);
+                *reinterpret_cast<bf16x4_t *>(op + db * 32 + g4 * 8 + grp * 4) = o4;
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path: a correctness path with fp32 arithmetic throughout. A workgroup
+// of 128 lanes owns 64 query rows of one head; each row is shared by two
+// adjacent lanes that each hold half of the head dimension.
+// ---------------------------------------------------------------------------
+
+constexpr int kF32Rows = 64;
+constexpr int kF32Keys = 32;
+
+struct AttnF32Args {
+    const float *q;
+    const float *k;
+    const float *v;
+    float *out;
+    int64_t S;
+    int64_t N;
+    int64_t Mq;
+    int32_t heads;
+    float scale;       // 1 / sqrt(d)
+    int32_t kf[kMaxFrames];
+};
+
+template <int D>
+__global__ __launch_bounds__(2 * kF32Rows) void attn_f32_kernel(const AttnF32Args a) {
+    constexpr int HD = D / 2;
+    __shared__ float ks[kF32Keys][D];
+    __shared__ float vs[kF32Keys][D];
+    const int head = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int half = tid & 1;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * kF32Rows + (tid >> 1);
+    const int64_t rs = static_cast<int64_t>(a.heads) * D;
+
+    float qv[HD], o[HD];
+    if (row < a.Mq) {
+        const int64_t f = row / a.N;
+        const int64_t tok = static_cast<int64_t>(a.kf[f]) * a.N + (row - f * a.N);
+        const float *qp = a.q + tok * rs + static_cast<int64_t>(head) * D + half * HD;
+#pragma unroll
+        for (int c = 0; c < HD; ++c) qv[c] = qp[c];
+    } else {
+#pragma unroll
+        for (int c = 0; c < HD; ++c) qv[c] = 0.0f;
+    }
+#pragma unroll
+    for (int c = 0; c < HD; ++c) o[c] = 0.0f;
+    float m = -__builtin_huge_valf(), l = 0.0f;
+
+    for (int64_t j0 = 0; j0 < a.S; j0 += kF32Keys) {
+        __syncthreads();
+        for (int i = tid; i < kF32Keys * D; i += 2 * kF32Rows) {
+            const int key = i / D, c = i % D;
+            const int64_t j = j0 + key;
+            const int64_t off = j * rs + static_cast<int64_t>(head) * D + c;
+            ks[key][c] = j < a.S ? a.k[off] : 0.0f;
+            vs[key][c] = j < a.S ? a.v[off] : 0.0f;
+        }
+        __syncthreads();
+        float s[kF32Keys];
+        float mt = -__builtin_huge_valf();
+#pragma unroll
+        for (int jj = 0; jj < kF32Keys; ++jj) {
+            float part = 0.0f;
+#pragma unroll
+            for (int c = 0; c < HD; ++c) part = fmaf(qv[c], ks[jj][half * HD + c], part);
+            const float dot = part + __shfl_xor(part, 1);
+            s[jj] = (j0 + jj < a.S) ? dot * a.scale : -__builtin_huge_valf();
+            mt = fmaxf(mt, s[jj]);
+        }
+        const float m_new = fmaxf(m, mt);
+        const float corr = expf(m - m_new);
+        l *= corr;
+#pragma unroll
+        for (int c = 0; c < HD; ++c) o[c] *= corr;
+#pragma unroll
+        for (int jj = 0; jj < kF32Keys; ++jj) {
+            const float p = expf(s[jj] - m_new);
+            l += p;
+#pragma unroll
+            for (int c = 0; c < HD; ++c) o[c] = fmaf(p, vs[jj][half * HD + c], o[c]);
+        }
+        m = m_new;
+    }
+    if (row < a.Mq) {
+        float *op = a.out + row * rs + static_cast<int64_t>(head) * D + half * HD;
+        const float inv = 1.0f / l;
+#pragma unroll
+        for (int c = 0; c < HD; ++c) op[c] = o[c] * inv;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
+    const int64_t Mq = static_cast<int64_t>(p.M) * p.N;
+    if (p.dtype == RF_BF16) {
+        AttnKArgs a{};
+        a.q = static_cast<const __bf16 *>(p.q);
+        a.k = static_cast<const __bf16 *>(p.k);
+        a.v = static_cast<const __bf16 *>(p.v);
+        a.out = static_cast<__bf16 *>(p.out);
+        a.S = p.S;
+        a.N = p.N;
+        a.Mq = Mq;
+        a.heads = p.heads;
+        const int64_t nq = (Mq + kBr - 1) / kBr;
+        const int64_t total = nq * p.heads;
+        const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+        if (total > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
+        a.n_qtiles = static_cast<int32_t>(nq);
+        a.total_tiles = static_cast<int32_t>(total);
+        a.per_xcd = static_cast<int32_t>(per_xcd);
+        a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(p.head_dim)));
+        for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
+        const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds)), block(kThreads);
+        if (p.head_dim == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, stream, a);
+        else hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, stream, a);
+        return hipGetLastError();
+    }
+    AttnF32Args a{};
+    a.q = static_cast<const float *>(p.q);
+    a.k = static_cast<const float *>(p.k);
+    a.v = static_cast<const float *>(p.v);
+    a.out = static_cast<float *>(p.out);
+    a.S = p.S;
+    a.N = p.N;
+    a.Mq = Mq;
+    a.heads = p.heads;
+    a.scale = static_cast<float>(1.0 / sqrt(static_cast<double>(p.head_dim)));
+    for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
+    const int64_t nq = (Mq + kF32Rows - 1) / kF32Rows;
+    if (nq > 0x7fffffffLL || p.heads > 65535) return hipErrorInvalidConfiguration;
+    const dim3 grid(static_cast<uint32_t>(nq), static_cast<uint32_t>(p.heads)), block(2 * kF32Rows);
+    if (p.head_dim == 128) hipLaunchKernelGGL(attn_f32_kernel<128>, grid, block, 0, stream, a);
+    else hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace rf
