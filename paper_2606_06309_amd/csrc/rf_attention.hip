@@ -35,8 +35,13 @@ namespace rf {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Data moves as 32-bit words; bf16 vectors are only ever formed by a
+// whole-vector bitcast of a u32x4 right before a matrix instruction.
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
@@ -47,10 +52,10 @@ constexpr int kVPad = 4;           // bf16 padding per V^T row in LDS (row = 136
 constexpr int kXcds = 8;
 
 struct AttnKArgs {
-    const __bf16 *q;
-    const __bf16 *k;
-    const __bf16 *v;
-    __bf16 *out;
+    const uint16_t *q;
+    const uint16_t *k;
+    const uint16_t *v;
+    uint16_t *out;
     int64_t S;
     int64_t N;
     int64_t Mq;
@@ -64,16 +69,24 @@ struct AttnKArgs {
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Two floats -> two bf16 (round to nearest even) packed low-first in a word.
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+    const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ inline bf16x8_t as_bf16x8(u32x4_t w) { return __builtin_bit_cast(bf16x8_t, w); }
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) {
-    constexpr int kKRow = D + kKPad;
+    constexpr int kKRow = D + kKPad;                    // bf16 elements
     constexpr int kVRow = kBc + kVPad;
     constexpr int kKChunks = kBc * D / 8 / kThreads;    // 16-byte K chunks per thread
     constexpr int kVChunks = kBc * D / 16 / kThreads;   // (2 keys x 8 dims) V chunks per thread
     static_assert(kKChunks >= 1 && kVChunks >= 1, "tile too small for the workgroup");
 
-    __shared__ __attribute__((aligned(16))) __bf16 ks[kBc * kKRow];
-    __shared__ __attribute__((aligned(16))) __bf16 vt[D * kVRow];
+    __shared__ __attribute__((aligned(16))) uint16_t ks[kBc * kKRow];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[D * kVRow];
 
     const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
     if (tile >= a.total_tiles) return;
@@ -86,18 +99,16 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
 
     // ---- query fragments: B operand of S^T = K Q^T (fused keyframe gather) ----
     const int64_t row = static_cast<int64_t>(qt) * kBr + wave * 32 + col;
-    bf16x8_t qf[D / 16];
+    u32x4_t qf[D / 16];
     if (row < a.Mq) {
         const int64_t f = row / a.N;
         const int64_t tok = static_cast<int64_t>(a.kf[f]) * a.N + (row - f * a.N);
-        const __bf16 *qp = a.q + tok * rs + static_cast<int64_t>(head) * D + grp * 8;
+        const uint16_t *qp = a.q + tok * rs + static_cast<int64_t>(head) * D + grp * 8;
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t *>(qp + kk * 16);
+        for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *reinterpret_cast<const u32x4_t *>(qp + kk * 16);
     } else {
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qf[kk][e] = static_cast<__bf16>(0.0f);
+        for (int kk = 0; kk < D / 16; ++kk) qf[kk] = u32x4_t{0u, 0u, 0u, 0u};
     }
 
     f32x16_t oacc[D / 32];
@@ -108,13 +119,11 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     float m_run = -__builtin_huge_valf();   // running max, log2 domain
     float l_run = 0.0f;                     // this lane's partial row sum
 
-    const __bf16 *kbase = a.k + static_cast<int64_t>(head) * D;
-    const __bf16 *vbase = a.v + static_cast<int64_t>(head) * D;
+    const uint16_t *kbase = a.k + static_cast<int64_t>(head) * D;
+    const uint16_t *vbase = a.v + static_cast<int64_t>(head) * D;
+    const u32x4_t zero4 = {0u, 0u, 0u, 0u};
 
-    bf16x8_t kreg[kKChunks], vreg0[kVChunks], vreg1[kVChunks];
-    bf16x8_t zero8;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) zero8[e] = static_cast<__bf16>(0.0f);
+    u32x4_t kreg[kKChunks], vreg0[kVChunks], vreg1[kVChunks];
 
     auto load_tile = [&](int64_t j0) {
 #pragma unroll
@@ -122,15 +131,15 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
             const int c = tid + i * kThreads;
             const int key = c / (D / 8), c8 = c % (D / 8);
             const int64_t j = j0 + key;
-            kreg[i] = j < a.S ? *reinterpret_cast<const bf16x8_t *>(kbase + j * rs + c8 * 8) : zero8;
+            kreg[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(kbase + j * rs + c8 * 8) : zero4;
         }
 #pragma unroll
         for (int i = 0; i < kVChunks; ++i) {
             const int p = tid + i * kThreads;
             const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
             const int64_t j = j0 + 2 * kp;
-            vreg0[i] = j < a.S ? *reinterpret_cast<const bf16x8_t *>(vbase + j * rs + c8 * 8) : zero8;
-            vreg1[i] = j + 1 < a.S ? *reinterpret_cast<const bf16x8_t *>(vbase + (j + 1) * rs + c8 * 8) : zero8;
+            vreg0[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + j * rs + c8 * 8) : zero4;
+            vreg1[i] = j + 1 < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + (j + 1) * rs + c8 * 8) : zero4;
         }
     };
     auto store_tile = [&]() {
@@ -138,18 +147,20 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
         for (int i = 0; i < kKChunks; ++i) {
             const int c = tid + i * kThreads;
             const int key = c / (D / 8), c8 = c % (D / 8);
-            *reinterpret_cast<bf16x8_t *>(&ks[key * kKRow + c8 * 8]) = kreg[i];
+            *reinterpret_cast<u32x4_t *>(&ks[key * kKRow + c8 * 8]) = kreg[i];
         }
 #pragma unroll
         for (int i = 0; i < kVChunks; ++i) {
             const int p = tid + i * kThreads;
             const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
+            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[(c8 * 8) * kVRow + 2 * kp]);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                // keys 2kp and 2kp+1 of dimension c8*8+e, adjacent in the transposed row
-                const uint32_t lo = __builtin_bit_cast(uint16_t, vreg0[i][e]);
-                const uint32_t hi = __builtin_bit_cast(uint16_t, vreg1[i][e]);
-                *reinterpret_cast<uint32_t *>(&vt[(c8 * 8 + e) * kVRow + 2 * kp]) = lo | (hi << 16);
+            for (int w = 0; w < 4; ++w) {
+                // word w holds dims 2w (low half) and 2w+1 (high half) of one key;
+                // the transposed row of a dim holds keys 2kp (low) and 2kp+1 (high)
+                const uint32_t x0 = vreg0[i][w], x1 = vreg1[i][w];
+                dst[(2 * w) * (kVRow / 2)] = (x0 & 0xffffu) | (x1 << 16);
+                dst[(2 * w + 1) * (kVRow / 2)] = (x0 >> 16) | (x1 & 0xffff0000u);
             }
         }
     };
@@ -163,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
         __syncthreads();
         if (t + 1 < ntiles) load_tile((t + 1) * kBc);   // in flight during this tile's math
 
-        // ---- S^T = K Q^T : two 32-key blocks ----
+        // ---- S^T = K Q^T : 32-key blocks ----
         f32x16_t sacc[kBc / 32];
 #pragma unroll
         for (int b = 0; b < kBc / 32; ++b) {
@@ -171,9 +182,10 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
             for (int r = 0; r < 16; ++r) sacc[b][r] = 0.0f;
 #pragma unroll
             for (int kk = 0; kk < D / 16; ++kk) {
-                const bf16x8_t kfrag =
-                    *reinterpret_cast<const bf16x8_t *>(&ks[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
-                sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag, qf[kk], sacc[b], 0, 0, 0);
+                const u32x4_t kw =
+                    *reinterpret_cast<const u32x4_t *>(&ks[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
+                sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kw), as_bf16x8(qf[kk]),
+                                                                  sacc[b], 0, 0, 0);
             }
         }
         // accumulator r of block b holds key b*32 + (r/4)*8 + grp*4 + r%4 for query `col`
@@ -200,15 +212,18 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
         const float corr = fast_exp2(m_run - m_new);
         m_run = m_new;
 
-        bf16x8_t pb[kBc / 16];
+        // probabilities, packed as the B operand of O^T = V^T P^T:
+        // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2
+        u32x4_t pw[kBc / 16];
         float ls = 0.0f;
 #pragma unroll
         for (int b = 0; b < kBc / 32; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = fast_exp2(fmaf(sacc[b][r], sl2, -m_new));
-                ls += p;
-                pb[b * 2 + r / 8][r % 8] = static_cast<__bf16>(p);
+            for (int r = 0; r < 16; r += 2) {
+                const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_new));
+                const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_new));
+                ls += p0 + p1;
+                pw[b * 2 + r / 8][(r % 8) / 2] = pack_bf16x2(p0, p1);
             }
         l_run = fmaf(l_run, corr, ls);
 #pragma unroll
@@ -222,11 +237,12 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
             const int key0 = (c / 2) * 32 + (c % 2) * 16 + grp * 4;   // operand elements 0..3
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
-                const __bf16 *vrow = &vt[(db * 32 + col) * kVRow];
-                const bf16x4_t lo = *reinterpret_cast<const bf16x4_t *>(vrow + key0);
-                const bf16x4_t hi = *reinterpret_cast<const bf16x4_t *>(vrow + key0 + 8);
-                const bf16x8_t vfrag = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag, pb[c], oacc[db], 0, 0, 0);
+                const uint16_t *vrow = &vt[(db * 32 + col) * kVRow];
+                const u32x2_t lo = *reinterpret_cast<const u32x2_t *>(vrow + key0);
+                const u32x2_t hi = *reinterpret_cast<const u32x2_t *>(vrow + key0 + 8);
+                const u32x4_t vw = {lo[0], lo[1], hi[0], hi[1]};
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vw), as_bf16x8(pw[c]),
+                                                                   oacc[db], 0, 0, 0);
             }
         }
     }
@@ -235,16 +251,16 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     l_run += __shfl_xor(l_run, 32);
     if (row < a.Mq) {
         const float inv = 1.0f / l_run;
-        __bf16 *op = a.out + row * rs + static_cast<int64_t>(head) * D;
+        uint16_t *op = a.out + row * rs + static_cast<int64_t>(head) * D;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
 #pragma unroll
             for (int g4 = 0; g4 < 4; ++g4) {
                 // accumulator r holds dimension db*32 + (r/4)*8 + grp*4 + r%4
-                bf16x4_t o4;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) o4[e] = static_cast<__bf16>(oacc[db][g4 * 4 + e] * inv);
-                *reinterpret_cast<bf16x4_t *>(op + db * 32 + g4 * 8 + grp * 4) = o4;
+                const int r = g4 * 4;
+                const u32x2_t w = {pack_bf16x2(oacc[db][r] * inv, oacc[db][r + 1] * inv),
+                                   pack_bf16x2(oacc[db][r + 2] * inv, oacc[db][r + 3] * inv)};
+                *reinterpret_cast<u32x2_t *>(op + db * 32 + g4 * 8 + grp * 4) = w;
             }
     }
 }
@@ -346,10 +362,10 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
     const int64_t Mq = static_cast<int64_t>(p.M) * p.N;
     if (p.dtype == RF_BF16) {
         AttnKArgs a{};
-        a.q = static_cast<const __bf16 *>(p.q);
-        a.k = static_cast<const __bf16 *>(p.k);
-        a.v = static_cast<const __bf16 *>(p.v);
-        a.out = static_cast<__bf16 *>(p.out);
+        a.q = static_cast<const uint16_t *>(p.q);
+        a.k = static_cast<const uint16_t *>(p.k);
+        a.v = static_cast<const uint16_t *>(p.v);
+        a.out = static_cast<uint16_t *>(p.out);
         a.S = p.S;
         a.N = p.N;
         a.Mq = Mq;
