@@ -83,6 +83,29 @@ def cpu_baseline(w, q, k, v, target_s):
                       f"all S={w.S} keys, fp64; {t:.1f} s"}
 
 
+def profiled_traffic(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, or None when there is none or the attention source has changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_bf16_{workload}_traffic.txt")
+    src = os.path.join(ROOT, "paper_2606_06309_amd", "csrc", "rf_attention.hip")
+    if not os.path.exists(path):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    fields = {}
+    for line in open(path):
+        if ":" in line:
+            key, _, val = line.partition(":")
+            fields[key.strip()] = val.strip()
+    if fields.get("attention source sha256") != sha:
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -158,7 +181,8 @@ def main():
                       "flop_per_launch": flop},
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": profiled_traffic(w.name)},
     }
 
     if not args.no_comparator:
