@@ -43,13 +43,28 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // Data moves as 32-bit words; bf16 vectors are only ever formed by a
 // whole-vector bitcast of a u32x4 right before a matrix instruction.
 
-constexpr int kWaves = 4;
+// Tunables (compile-time): waves per workgroup (each owns 32 query rows), keys
+// per LDS tile, and the log2-domain slack before the running max is rebased
+// (0: the reference is always the exact running max, so the largest
+// probability is exactly 1 and exactly representable in bf16).
+#ifndef RF_ATTN_WAVES
+#define RF_ATTN_WAVES 8
+#endif
+#ifndef RF_ATTN_BC
+#define RF_ATTN_BC 64
+#endif
+#ifndef RF_ATTN_RESCALE_SLACK
+#define RF_ATTN_RESCALE_SLACK 0.0f
+#endif
+
+constexpr int kWaves = RF_ATTN_WAVES;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
-constexpr int kBc = 64;            // keys per tile
+constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
 constexpr int kKPad = 8;           // bf16 padding per K row in LDS (row = 272 B at d=128)
-constexpr int kVPad = 4;           // bf16 padding per V^T row in LDS (row = 136 B)
+constexpr int kVPad = 4;           // bf16 padding per V^T row in LDS
 constexpr int kXcds = 8;
+static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
 
 struct AttnKArgs {
     const uint16_t *q;
@@ -77,16 +92,23 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ inline bf16x8_t as_bf16x8(u32x4_t w) { return __builtin_bit_cast(bf16x8_t, w); }
 
+// Per-tile pipeline with double-buffered LDS and one barrier per tile:
+//   global loads of tile t+1 -> registers   (in flight during the math)
+//   math on LDS buffer t%2
+//   registers -> LDS buffer (t+1)%2          (last read during tile t-1)
+//   barrier
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) {
-    constexpr int kKRow = D + kKPad;                    // bf16 elements
-    constexpr int kVRow = kBc + kVPad;
-    constexpr int kKChunks = kBc * D / 8 / kThreads;    // 16-byte K chunks per thread
-    constexpr int kVChunks = kBc * D / 16 / kThreads;   // (2 keys x 8 dims) V chunks per thread
-    static_assert(kKChunks >= 1 && kVChunks >= 1, "tile too small for the workgroup");
+    constexpr int kKRow = D + kKPad;                    // bf16 elements per K row
+    constexpr int kVRow = kBc + kVPad;                  // bf16 elements per V^T row
+    constexpr int kKTotal = kBc * D / 8;                // 16-byte K chunks per tile
+    constexpr int kVTotal = (kBc / 2) * (D / 8);        // (2 keys x 8 dims) V chunks per tile
+    constexpr int kKChunks = (kKTotal + kThreads - 1) / kThreads;
+    constexpr int kVChunks = (kVTotal + kThreads - 1) / kThreads;
+    constexpr int kNB = kBc / 32;                       // 32-key score blocks per tile
 
-    __shared__ __attribute__((aligned(16))) uint16_t ks[kBc * kKRow];
-    __shared__ __attribute__((aligned(16))) uint16_t vt[D * kVRow];
+    __shared__ __attribute__((aligned(16))) uint16_t ks[2][kBc * kKRow];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[2][D * kVRow];
 
     const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
     if (tile >= a.total_tiles) return;
@@ -116,8 +138,12 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
-    float m_run = -__builtin_huge_valf();   // running max, log2 domain
-    float l_run = 0.0f;                     // this lane's partial row sum
+    // m_run: reference max (log2 domain) the probabilities are taken against.
+    // It is rebased when the running max exceeds it by more than the slack, so
+    // p <= 2^slack; the final O / l does not depend on the reference. The
+    // accumulators are rescaled only on tiles where some lane rebased.
+    float m_run = -__builtin_huge_valf();
+    float l_run = 0.0f;   // this lane's partial row sum
 
     const uint16_t *kbase = a.k + static_cast<int64_t>(head) * D;
     const uint16_t *vbase = a.v + static_cast<int64_t>(head) * D;
@@ -129,6 +155,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
 #pragma unroll
         for (int i = 0; i < kKChunks; ++i) {
             const int c = tid + i * kThreads;
+            if (kKTotal % kThreads != 0 && c >= kKTotal) break;
             const int key = c / (D / 8), c8 = c % (D / 8);
             const int64_t j = j0 + key;
             kreg[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(kbase + j * rs + c8 * 8) : zero4;
@@ -136,24 +163,27 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
 #pragma unroll
         for (int i = 0; i < kVChunks; ++i) {
             const int p = tid + i * kThreads;
+            if (kVTotal % kThreads != 0 && p >= kVTotal) break;
             const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
             const int64_t j = j0 + 2 * kp;
             vreg0[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + j * rs + c8 * 8) : zero4;
             vreg1[i] = j + 1 < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + (j + 1) * rs + c8 * 8) : zero4;
         }
     };
-    auto store_tile = [&]() {
+    auto store_tile = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < kKChunks; ++i) {
             const int c = tid + i * kThreads;
+            if (kKTotal % kThreads != 0 && c >= kKTotal) break;
             const int key = c / (D / 8), c8 = c % (D / 8);
-            *reinterpret_cast<u32x4_t *>(&ks[key * kKRow + c8 * 8]) = kreg[i];
+            *reinterpret_cast<u32x4_t *>(&ks[buf][key * kKRow + c8 * 8]) = kreg[i];
         }
 #pragma unroll
         for (int i = 0; i < kVChunks; ++i) {
             const int p = tid + i * kThreads;
+            if (kVTotal % kThreads != 0 && p >= kVTotal) break;
             const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[(c8 * 8) * kVRow + 2 * kp]);
+            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[buf][(c8 * 8) * kVRow + 2 * kp]);
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 // word w holds dims 2w (low half) and 2w+1 (high half) of one key;
@@ -168,22 +198,24 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     const int64_t ntiles = (a.S + kBc - 1) / kBc;
     const float sl2 = a.scale_log2;
     load_tile(0);
+    store_tile(0);
+    __syncthreads();
     for (int64_t t = 0; t < ntiles; ++t) {
-        __syncthreads();   // every wave is done reading the previous tile
-        store_tile();
-        __syncthreads();
+        const int buf = static_cast<int>(t & 1);
         if (t + 1 < ntiles) load_tile((t + 1) * kBc);   // in flight during this tile's math
+        const uint16_t *kb = ks[buf];
+        const uint16_t *vb = vt[buf];
 
         // ---- S^T = K Q^T : 32-key blocks ----
-        f32x16_t sacc[kBc / 32];
+        f32x16_t sacc[kNB];
 #pragma unroll
-        for (int b = 0; b < kBc / 32; ++b) {
+        for (int b = 0; b < kNB; ++b) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) sacc[b][r] = 0.0f;
 #pragma unroll
             for (int kk = 0; kk < D / 16; ++kk) {
                 const u32x4_t kw =
-                    *reinterpret_cast<const u32x4_t *>(&ks[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
+                    *reinterpret_cast<const u32x4_t *>(&kb[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
                 sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kw), as_bf16x8(qf[kk]),
                                                                   sacc[b], 0, 0, 0);
             }
@@ -193,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
         const int64_t j0 = t * kBc;
         if (j0 + kBc > a.S) {
 #pragma unroll
-            for (int b = 0; b < kBc / 32; ++b)
+            for (int b = 0; b < kNB; ++b)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int64_t key = j0 + b * 32 + (r / 4) * 8 + grp * 4 + (r % 4);
@@ -201,43 +233,47 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
                 }
         }
 
-        // ---- online softmax (log2 domain) ----
+        // ---- online softmax (log2 domain) with a lazily rebased reference max ----
         float mx = -__builtin_huge_valf();
 #pragma unroll
-        for (int b = 0; b < kBc / 32; ++b)
+        for (int b = 0; b < kNB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[b][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * sl2);
-        const float corr = fast_exp2(m_run - m_new);
-        m_run = m_new;
+        mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+        const bool rebase = mx > m_run + RF_ATTN_RESCALE_SLACK;
+        if (__builtin_amdgcn_ballot_w64(rebase)) {   // wave-uniform branch, rarer as the max settles
+            const float m_new = rebase ? mx : m_run;
+            const float corr = fast_exp2(m_run - m_new);
+            m_run = m_new;
+            l_run *= corr;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[db][r] *= corr;
+        }
 
         // probabilities, packed as the B operand of O^T = V^T P^T:
         // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2
-        u32x4_t pw[kBc / 16];
+        u32x4_t pw[2 * kNB];
         float ls = 0.0f;
 #pragma unroll
-        for (int b = 0; b < kBc / 32; ++b)
+        for (int b = 0; b < kNB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; r += 2) {
-                const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_new));
-                const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_new));
+                const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_run));
+                const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_run));
                 ls += p0 + p1;
                 pw[b * 2 + r / 8][(r % 8) / 2] = pack_bf16x2(p0, p1);
             }
-        l_run = fmaf(l_run, corr, ls);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[db][r] *= corr;
+        l_run += ls;
 
         // ---- O^T += V^T P^T ----
 #pragma unroll
-        for (int c = 0; c < kBc / 16; ++c) {
+        for (int c = 0; c < 2 * kNB; ++c) {
             const int key0 = (c / 2) * 32 + (c % 2) * 16 + grp * 4;   // operand elements 0..3
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) {
-                const uint16_t *vrow = &vt[(db * 32 + col) * kVRow];
+                const uint16_t *vrow = &vb[(db * 32 + col) * kVRow];
                 const u32x2_t lo = *reinterpret_cast<const u32x2_t *>(vrow + key0);
                 const u32x2_t hi = *reinterpret_cast<const u32x2_t *>(vrow + key0 + 8);
                 const u32x4_t vw = {lo[0], lo[1], hi[0], hi[1]};
@@ -245,6 +281,9 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
                                                                    oacc[db], 0, 0, 0);
             }
         }
+
+        if (t + 1 < ntiles) store_tile(buf ^ 1);
+        __syncthreads();
     }
 
     // ---- epilogue: normalise, round to bf16, store the compact row ----
