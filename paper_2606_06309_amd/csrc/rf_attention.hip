@@ -41,12 +41,13 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Data moves as 32-bit words; bf16 vectors are only ever formed by a
-// whole-vector bitcast of a u32x4 right before a matrix instruction.
+// whole-vector bitcast of a u32x4 (or of one scalar word) right before the
+// instruction that consumes them.
 
 // Tunables (compile-time): waves per workgroup (each owns 32 query rows), keys
-// per LDS tile, and the log2-domain slack before the running max is rebased
-// (0: the reference is always the exact running max, so the largest
-// probability is exactly 1 and exactly representable in bf16).
+// per LDS tile, the log2-domain slack before the running max is rebased (0:
+// the reference is always the exact running max, so the largest probability
+// is exactly 1), and how many LDS fragments the matrix core reads ahead.
 #ifndef RF_ATTN_WAVES
 #define RF_ATTN_WAVES 8
 #endif
@@ -56,13 +57,19 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 #ifndef RF_ATTN_RESCALE_SLACK
 #define RF_ATTN_RESCALE_SLACK 0.0f
 #endif
+#ifndef RF_ATTN_K_LEAD
+#define RF_ATTN_K_LEAD 4
+#endif
+#ifndef RF_ATTN_V_LEAD
+#define RF_ATTN_V_LEAD 3
+#endif
 
 constexpr int kWaves = RF_ATTN_WAVES;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
 constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
 constexpr int kKPad = 8;           // bf16 padding per K row in LDS (row = 272 B at d=128)
-constexpr int kVPad = 4;           // bf16 padding per V^T row in LDS
+constexpr int kVPad = 8;           // bf16 padding per V^T row in LDS (row = 144 B at 64 keys)
 constexpr int kXcds = 8;
 static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
 
@@ -82,7 +89,18 @@ struct AttnKArgs {
     int32_t kf[kMaxFrames];
 };
 
+// Word 3 of a raw (untyped, stride 0) buffer resource on gfx9-class GPUs.
+constexpr int kBufferWord3 = 0x00020000;
+
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// A pointer every lane holds the same value of, rebuilt from its first lane.
+__device__ __forceinline__ void *uniform_ptr(const void *p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<void *>((static_cast<uint64_t>(hi) << 32) | lo);
+}
 
 // Two floats -> two bf16 (round to nearest even) packed low-first in a word.
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
@@ -92,13 +110,106 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ inline bf16x8_t as_bf16x8(u32x4_t w) { return __builtin_bit_cast(bf16x8_t, w); }
 
+// lo + hi of a packed bf16 pair, accumulated in fp32 (v_dot2 against (1, 1)).
+__device__ __forceinline__ float add_bf16x2(uint32_t word, float acc) {
+    const bf16x2_t one = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, word), one, acc, false);
+}
+
+// Combine the values of lanes l and l ^ 32 with one VALU swap of the wave
+// halves: r[0] holds lanes 0..31 in both halves, r[1] lanes 32..63.
+__device__ __forceinline__ float halves_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// S^T = K Q^T for one tile of kNB 32-key blocks, with the K fragments read
+// from LDS through a ring RF_ATTN_K_LEAD fragments ahead of the matrix core.
+// The scheduling groups pin that order: LEAD reads, then (1 MFMA, 1 read)
+// pairs, then the last LEAD MFMAs.
+template <int D, int kNB, int kKRow>
+__device__ __forceinline__ void scores_tile(const uint16_t *kb, const u32x4_t (&qf)[D / 16],
+                                            f32x16_t (&sacc)[kNB], int col, int grp) {
+    constexpr int kSteps = D / 16;
+    constexpr int kNF = kNB * kSteps;
+    constexpr int kLead = RF_ATTN_K_LEAD < kNF ? RF_ATTN_K_LEAD : kNF;
+    u32x4_t ring[kLead];
+    auto rd = [&](int i) {
+        const int b = i / kSteps, kk = i % kSteps;
+        return *reinterpret_cast<const u32x4_t *>(&kb[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
+    };
+#pragma unroll
+    for (int i = 0; i < kLead; ++i) ring[i] = rd(i);
+#pragma unroll
+    for (int i = 0; i < kNF; ++i) {
+        const int b = i / kSteps, kk = i % kSteps;
+        const f32x16_t c = kk == 0 ? f32x16_t{} : sacc[b];
+        sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ring[i % kLead]), as_bf16x8(qf[kk]), c,
+                                                          0, 0, 0);
+        if (i + kLead < kNF) ring[i % kLead] = rd(i + kLead);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kLead, 0);
+#pragma unroll
+    for (int i = 0; i < kNF - kLead; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
+}
+
+// Column of key k in a transposed V row: within every 16-key group the middle
+// two 4-key quarters are swapped, so the 8 keys one lane contributes to an A
+// operand (keys grp*4 + 0..3 and 8 + grp*4 + 0..3 of the group, following the
+// score accumulator layout) sit in 8 consecutive columns: one 128-bit read.
+__host__ __device__ constexpr int vt_column(int k) {
+    return (k & ~15) | ((((k >> 2) & 3) == 1 ? 2 : (((k >> 2) & 3) == 2 ? 1 : ((k >> 2) & 3))) << 2) | (k & 3);
+}
+
+// O^T += V^T P^T for one tile; each A operand is one 128-bit read of the
+// transposed V tile, issued RF_ATTN_V_LEAD operands ahead.
+template <int D, int kNB, int kVRow>
+__device__ __forceinline__ void pv_tile(const uint16_t *vb, const u32x4_t (&pw)[2 * kNB],
+                                        f32x16_t (&oacc)[D / 32], int col, int grp) {
+    constexpr int kNF = 2 * kNB * (D / 32);
+    constexpr int kLead = RF_ATTN_V_LEAD < kNF ? RF_ATTN_V_LEAD : kNF;
+    u32x4_t ring[kLead];
+    auto rd = [&](int i) {
+        const int c = i / (D / 32), db = i % (D / 32);
+        return *reinterpret_cast<const u32x4_t *>(&vb[(db * 32 + col) * kVRow + c * 16 + grp * 8]);
+    };
+#pragma unroll
+    for (int i = 0; i < kLead; ++i) ring[i] = rd(i);
+#pragma unroll
+    for (int i = 0; i < kNF; ++i) {
+        const int c = i / (D / 32), db = i % (D / 32);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(ring[i % kLead]), as_bf16x8(pw[c]),
+                                                           oacc[db], 0, 0, 0);
+        if (i + kLead < kNF) ring[i % kLead] = rd(i + kLead);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, kLead, 0);
+#pragma unroll
+    for (int i = 0; i < kNF - kLead; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
+}
+
 // Per-tile pipeline with double-buffered LDS and one barrier per tile:
 //   global loads of tile t+1 -> registers   (in flight during the math)
 //   math on LDS buffer t%2
 //   registers -> LDS buffer (t+1)%2          (last read during tile t-1)
 //   barrier
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) {
+// kBuf: K/V staging through raw buffer loads whose resource is rebased per
+// tile in scalar registers, so the hardware range check zero-fills keys >= S
+// and no per-tile vector address arithmetic is needed (tensors below 2 GiB).
+template <int D, bool kBuf>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_bf16_kernel(const AttnKArgs a) {
     constexpr int kKRow = D + kKPad;                    // bf16 elements per K row
     constexpr int kVRow = kBc + kVPad;                  // bf16 elements per V^T row
     constexpr int kKTotal = kBc * D / 8;                // 16-byte K chunks per tile
@@ -106,9 +217,11 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     constexpr int kKChunks = (kKTotal + kThreads - 1) / kThreads;
     constexpr int kVChunks = (kVTotal + kThreads - 1) / kThreads;
     constexpr int kNB = kBc / 32;                       // 32-key score blocks per tile
+    constexpr int kKBufs = 2;                           // K tile buffers (see the loop below)
+    constexpr int kVBufs = 2;                           // V tile buffers
 
-    __shared__ __attribute__((aligned(16))) uint16_t ks[2][kBc * kKRow];
-    __shared__ __attribute__((aligned(16))) uint16_t vt[2][D * kVRow];
+    __shared__ __attribute__((aligned(16))) uint16_t ks[kKBufs][kBc * kKRow];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[kVBufs][D * kVRow];
 
     const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
     if (tile >= a.total_tiles) return;
@@ -148,78 +261,103 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
     const uint16_t *kbase = a.k + static_cast<int64_t>(head) * D;
     const uint16_t *vbase = a.v + static_cast<int64_t>(head) * D;
     const u32x4_t zero4 = {0u, 0u, 0u, 0u};
+    // bytes from a head's first element to one past the last element it owns
+    const int64_t head_bytes = ((a.S - 1) * rs + D) * 2;
 
     u32x4_t kreg[kKChunks], vreg0[kVChunks], vreg1[kVChunks];
 
     auto load_tile = [&](int64_t j0) {
+        if constexpr (kBuf) {
+            // scalar rebase: the resource starts at key j0, its range ends at the head's last key.
+            // The inputs are workgroup-uniform; readfirstlane states that to the compiler so the
+            // resource lives in scalar registers (no per-load uniformity loop).
+            const int64_t off = j0 * rs * 2;
+            const int32_t rec = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(head_bytes - off));
+            const __amdgpu_buffer_rsrc_t kr =
+                __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + j0 * rs), 0, rec, kBufferWord3);
+            const __amdgpu_buffer_rsrc_t vr =
+                __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(vbase + j0 * rs), 0, rec, kBufferWord3);
 #pragma unroll
-        for (int i = 0; i < kKChunks; ++i) {
-            const int c = tid + i * kThreads;
-            if (kKTotal % kThreads != 0 && c >= kKTotal) break;
-            const int key = c / (D / 8), c8 = c % (D / 8);
-            const int64_t j = j0 + key;
-            kreg[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(kbase + j * rs + c8 * 8) : zero4;
-        }
+            for (int i = 0; i < kKChunks; ++i) {
+                const int c = tid + i * kThreads;
+                if (kKTotal % kThreads != 0 && c >= kKTotal) break;
+                const int key = c / (D / 8), c8 = c % (D / 8);
+                kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    kr, static_cast<int32_t>((key * rs + c8 * 8) * 2), 0, 0);
+            }
 #pragma unroll
-        for (int i = 0; i < kVChunks; ++i) {
-            const int p = tid + i * kThreads;
-            if (kVTotal % kThreads != 0 && p >= kVTotal) break;
-            const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-            const int64_t j = j0 + 2 * kp;
-            vreg0[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + j * rs + c8 * 8) : zero4;
-            vreg1[i] = j + 1 < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + (j + 1) * rs + c8 * 8) : zero4;
+            for (int i = 0; i < kVChunks; ++i) {
+                const int p = tid + i * kThreads;
+                if (kVTotal % kThreads != 0 && p >= kVTotal) break;
+                const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
+                const int32_t o = static_cast<int32_t>((2 * kp * rs + c8 * 8) * 2);
+                vreg0[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, o, 0, 0);
+                vreg1[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, o + static_cast<int32_t>(rs * 2), 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < kKChunks; ++i) {
+                const int c = tid + i * kThreads;
+                if (kKTotal % kThreads != 0 && c >= kKTotal) break;
+                const int key = c / (D / 8), c8 = c % (D / 8);
+                const int64_t j = j0 + key;
+                kreg[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(kbase + j * rs + c8 * 8) : zero4;
+            }
+#pragma unroll
+            for (int i = 0; i < kVChunks; ++i) {
+                const int p = tid + i * kThreads;
+                if (kVTotal % kThreads != 0 && p >= kVTotal) break;
+                const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
+                const int64_t j = j0 + 2 * kp;
+                vreg0[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + j * rs + c8 * 8) : zero4;
+                vreg1[i] =
+                    j + 1 < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + (j + 1) * rs + c8 * 8) : zero4;
+            }
         }
     };
-    auto store_tile = [&](int buf) {
+    auto store_tile = [&](int kbuf, int vbuf) {
 #pragma unroll
         for (int i = 0; i < kKChunks; ++i) {
             const int c = tid + i * kThreads;
             if (kKTotal % kThreads != 0 && c >= kKTotal) break;
             const int key = c / (D / 8), c8 = c % (D / 8);
-            *reinterpret_cast<u32x4_t *>(&ks[buf][key * kKRow + c8 * 8]) = kreg[i];
+            *reinterpret_cast<u32x4_t *>(&ks[kbuf][key * kKRow + c8 * 8]) = kreg[i];
         }
 #pragma unroll
         for (int i = 0; i < kVChunks; ++i) {
             const int p = tid + i * kThreads;
             if (kVTotal % kThreads != 0 && p >= kVTotal) break;
             const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[buf][(c8 * 8) * kVRow + 2 * kp]);
+            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[vbuf][(c8 * 8) * kVRow + vt_column(2 * kp)]);
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 // word w holds dims 2w (low half) and 2w+1 (high half) of one key;
-                // the transposed row of a dim holds keys 2kp (low) and 2kp+1 (high)
+                // the transposed row of a dim holds keys 2kp (low) and 2kp+1
+                // (high) side by side (vt_column keeps even/odd key pairs adjacent)
                 const uint32_t x0 = vreg0[i][w], x1 = vreg1[i][w];
-                dst[(2 * w) * (kVRow / 2)] = (x0 & 0xffffu) | (x1 << 16);
-                dst[(2 * w + 1) * (kVRow / 2)] = (x0 >> 16) | (x1 & 0xffff0000u);
+                dst[(2 * w) * (kVRow / 2)] = __builtin_amdgcn_perm(x1, x0, 0x05040100u);
+                dst[(2 * w + 1) * (kVRow / 2)] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
             }
         }
     };
 
+    // Per-tile pipeline with double-buffered LDS and one barrier per tile:
+    //   global loads of tile t+1 -> registers   (in flight during the math)
+    //   math on LDS buffer t%2
+    //   registers -> LDS buffer (t+1)%2          (last read during tile t-1)
+    //   barrier
     const int64_t ntiles = (a.S + kBc - 1) / kBc;
     const float sl2 = a.scale_log2;
     load_tile(0);
-    store_tile(0);
+    store_tile(0, 0);
     __syncthreads();
     for (int64_t t = 0; t < ntiles; ++t) {
         const int buf = static_cast<int>(t & 1);
         if (t + 1 < ntiles) load_tile((t + 1) * kBc);   // in flight during this tile's math
-        const uint16_t *kb = ks[buf];
-        const uint16_t *vb = vt[buf];
 
         // ---- S^T = K Q^T : 32-key blocks ----
         f32x16_t sacc[kNB];
-#pragma unroll
-        for (int b = 0; b < kNB; ++b) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) sacc[b][r] = 0.0f;
-#pragma unroll
-            for (int kk = 0; kk < D / 16; ++kk) {
-                const u32x4_t kw =
-                    *reinterpret_cast<const u32x4_t *>(&kb[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
-                sacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kw), as_bf16x8(qf[kk]),
-                                                                  sacc[b], 0, 0, 0);
-            }
-        }
+        scores_tile<D, kNB, kKRow>(ks[buf], qf, sacc, col, grp);
         // accumulator r of block b holds key b*32 + (r/4)*8 + grp*4 + r%4 for query `col`
 
         const int64_t j0 = t * kBc;
@@ -233,13 +371,13 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
                 }
         }
 
-        // ---- online softmax (log2 domain) with a lazily rebased reference max ----
+        // ---- online softmax (log2 domain) ----
         float mx = -__builtin_huge_valf();
 #pragma unroll
         for (int b = 0; b < kNB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[b][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+        mx = halves_max(mx) * sl2;
         const bool rebase = mx > m_run + RF_ATTN_RESCALE_SLACK;
         if (__builtin_amdgcn_ballot_w64(rebase)) {   // wave-uniform branch, rarer as the max settles
             const float m_new = rebase ? mx : m_run;
@@ -253,7 +391,8 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
         }
 
         // probabilities, packed as the B operand of O^T = V^T P^T:
-        // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2
+        // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2.
+        // The row sum adds the bf16-rounded values the matrix core consumes.
         u32x4_t pw[2 * kNB];
         float ls = 0.0f;
 #pragma unroll
@@ -262,32 +401,21 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(const AttnKArgs a) 
             for (int r = 0; r < 16; r += 2) {
                 const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_run));
                 const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_run));
-                ls += p0 + p1;
-                pw[b * 2 + r / 8][(r % 8) / 2] = pack_bf16x2(p0, p1);
+                const uint32_t word = pack_bf16x2(p0, p1);
+                ls = add_bf16x2(word, ls);
+                pw[b * 2 + r / 8][(r % 8) / 2] = word;
             }
         l_run += ls;
 
         // ---- O^T += V^T P^T ----
-#pragma unroll
-        for (int c = 0; c < 2 * kNB; ++c) {
-            const int key0 = (c / 2) * 32 + (c % 2) * 16 + grp * 4;   // operand elements 0..3
-#pragma unroll
-            for (int db = 0; db < D / 32; ++db) {
-                const uint16_t *vrow = &vb[(db * 32 + col) * kVRow];
-                const u32x2_t lo = *reinterpret_cast<const u32x2_t *>(vrow + key0);
-                const u32x2_t hi = *reinterpret_cast<const u32x2_t *>(vrow + key0 + 8);
-                const u32x4_t vw = {lo[0], lo[1], hi[0], hi[1]};
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vw), as_bf16x8(pw[c]),
-                                                                   oacc[db], 0, 0, 0);
-            }
-        }
+        pv_tile<D, kNB, kVRow>(vt[buf], pw, oacc, col, grp);
 
-        if (t + 1 < ntiles) store_tile(buf ^ 1);
+        if (t + 1 < ntiles) store_tile(buf ^ 1, buf ^ 1);
         __syncthreads();
     }
 
     // ---- epilogue: normalise, round to bf16, store the compact row ----
-    l_run += __shfl_xor(l_run, 32);
+    l_run = halves_sum(l_run);
     if (row < a.Mq) {
         const float inv = 1.0f / l_run;
         uint16_t *op = a.out + row * rs + static_cast<int64_t>(head) * D;
@@ -419,8 +547,15 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(p.head_dim)));
         for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
         const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds)), block(kThreads);
-        if (p.head_dim == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, stream, a);
-        else hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, stream, a);
+        // buffer addressing covers a head's keys with 32-bit byte offsets
+        const bool buf = p.S * p.heads * p.head_dim * 2 < 0x7fffffffLL;
+        if (p.head_dim == 128) {
+            if (buf) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, stream, a);
+        } else {
+            if (buf) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, stream, a);
+        }
         return hipGetLastError();
     }
     AttnF32Args a{};
