@@ -5,7 +5,7 @@
 // values of all T frames. Per head: out = softmax(Q_kf K^T / sqrt(d)) V.
 //
 // bf16 kernel design:
-//  * A workgroup of 4 waves owns one (head, 128-row query tile); each wave
+//  * A workgroup of 8 waves owns one (head, 256-row query tile); each wave
 //    owns 32 query rows. Query rows are gathered straight from the keyframe
 //    tokens (row r reads token kf[r / N] * N + r % N), so the gather is fused
 //    and non-keyframe query rows are never read.
@@ -17,14 +17,17 @@
 //    exchange with the lane 32 apart.
 //  * The probabilities are already in the B-operand layout of the second
 //    product, O^T = V^T P^T: the lane's 16 accumulators become two bf16x8
-//    operands without any data movement. V is staged transposed in LDS
-//    ([d][key]) so each A operand is two 64-bit LDS reads; the key order
+//    operands without any data movement. The V^T A operands are read from
+//    the natural [key][dim] V tile with transposing LDS reads; the key order
 //    inside an operand follows the accumulator layout (a reduction index may
 //    be permuted freely as long as both operands agree).
+//  * K and V tiles of 64 keys go from HBM straight into LDS (buffer loads
+//    with an LDS destination: no staging registers, no LDS write
+//    instructions), double-buffered so the next tile streams in while the
+//    current one is computed; the buffer range check zero-fills keys >= S and
+//    the last tile masks their scores.
 //  * Online softmax in the log2 domain with fp32 state; P is rounded to bf16
-//    for the matrix cores, the row sum uses the unrounded fp32 values.
-//  * K/V tiles of 64 keys are prefetched into registers while the current
-//    tile is computed; the last tile masks keys >= S.
+//    for the matrix cores and the row sum adds those same rounded values.
 //  * Workgroup ids are mapped XCD-aware: consecutive ids go round-robin to the
 //    8 XCDs, so tile = (id % 8) * per_xcd + id / 8 gives each XCD a contiguous,
 //    head-major range of tiles and the workgroups resident on one XCD stream
@@ -68,8 +71,6 @@ constexpr int kWaves = RF_ATTN_WAVES;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
 constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
-constexpr int kKPad = 8;           // bf16 padding per K row in LDS (row = 272 B at d=128)
-constexpr int kVPad = 8;           // bf16 padding per V^T row in LDS (row = 144 B at 64 keys)
 constexpr int kXcds = 8;
 static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
 
@@ -127,20 +128,55 @@ __device__ __forceinline__ float halves_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// S^T = K Q^T for one tile of kNB 32-key blocks, with the K fragments read
-// from LDS through a ring RF_ATTN_K_LEAD fragments ahead of the matrix core.
-// The scheduling groups pin that order: LEAD reads, then (1 MFMA, 1 read)
-// pairs, then the last LEAD MFMAs.
-template <int D, int kNB, int kKRow>
-__device__ __forceinline__ void scores_tile(const uint16_t *kb, const u32x4_t (&qf)[D / 16],
-                                            f32x16_t (&sacc)[kNB], int col, int grp) {
+// LDS tile layout. A tile holds kBc keys of one head, K and V each in natural
+// [key][dim] order with unpadded rows of 2*D bytes, so that the global->LDS
+// loads can write whole 1 KB wave-chunks at consecutive addresses (lane l of a
+// load lands at chunk + 16 l). Bank conflicts on the reads are removed by
+// permuting the 16-byte slots of each row with an XOR of a key-dependent mask:
+//   K: slot = chunk ^ kswz(key) makes the 16 lanes of one 128-bit read pass
+//      (16 consecutive keys, same chunk) hit 16 different slot positions of
+//      the 256-byte bank window;
+//   V: slot = chunk ^ vswz(key) makes the 32 lanes of one transposing 64-bit
+//      read pass (4 keys x 64 bytes) hit 8 different 32-byte positions.
+template <int D>
+struct TileLayout {
+    static constexpr int kRow = 2 * D;                 // bytes per key row
+    static constexpr int kSlots = kRow / 16;           // 16-byte slots per row
+    static constexpr int kRowsPerWin = 256 / kRow;     // rows per 256-byte bank window
+    static constexpr int kTileBytes = kBc * kRow;
+    static constexpr int kRowsPerLoad = 1024 / kRow;   // rows one wave-wide 16-byte load fills
+    static constexpr int kLoads = kTileBytes / 1024;   // wave-wide loads per tensor per tile
+    __host__ __device__ static constexpr int kswz(int key) { return (key / kRowsPerWin) % kSlots; }
+    __host__ __device__ static constexpr int vswz(int key) { return 4 * ((key / kRowsPerWin) % (kSlots / 4)); }
+};
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+// 16 bytes per lane from a buffer resource straight into LDS: lane l's bytes
+// land at dst + 16 l; offsets at or past the resource's range read as zero.
+// (Kept out of the kernel template: the host pass drops the launch stub of a
+// template that names this builtin.)
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, lds_void_t *dst, int voffset) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voffset, 0, 0, 0);
+}
+
+// S^T = K Q^T for one tile of kNB 32-key blocks. kofs[kk] is this lane's byte
+// offset of its K fragment for reduction step kk inside block 0. The K
+// fragments are read through a ring RF_ATTN_K_LEAD fragments ahead of the
+// matrix core; the scheduling groups pin that order: LEAD reads, then
+// (1 MFMA, 1 read) pairs, then the last LEAD MFMAs.
+template <int D, int kNB>
+__device__ __forceinline__ void scores_tile(const uint8_t *kb, const int (&kofs)[D / 16],
+                                            const u32x4_t (&qf)[D / 16], f32x16_t (&sacc)[kNB]) {
     constexpr int kSteps = D / 16;
     constexpr int kNF = kNB * kSteps;
     constexpr int kLead = RF_ATTN_K_LEAD < kNF ? RF_ATTN_K_LEAD : kNF;
     u32x4_t ring[kLead];
     auto rd = [&](int i) {
         const int b = i / kSteps, kk = i % kSteps;
-        return *reinterpret_cast<const u32x4_t *>(&kb[(b * 32 + col) * kKRow + kk * 16 + grp * 8]);
+        return *reinterpret_cast<const u32x4_t *>(kb + kofs[kk] + b * 32 * TileLayout<D>::kRow);
     };
 #pragma unroll
     for (int i = 0; i < kLead; ++i) ring[i] = rd(i);
@@ -161,25 +197,33 @@ __device__ __forceinline__ void scores_tile(const uint16_t *kb, const u32x4_t (&
     __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
 }
 
-// Column of key k in a transposed V row: within every 16-key group the middle
-// two 4-key quarters are swapped, so the 8 keys one lane contributes to an A
-// operand (keys grp*4 + 0..3 and 8 + grp*4 + 0..3 of the group, following the
-// score accumulator layout) sit in 8 consecutive columns: one 128-bit read.
-__host__ __device__ constexpr int vt_column(int k) {
-    return (k & ~15) | ((((k >> 2) & 3) == 1 ? 2 : (((k >> 2) & 3) == 2 ? 1 : ((k >> 2) & 3))) << 2) | (k & 3);
+// One A operand of O^T = V^T P^T: dims db*32 + (lane % 32) of the 16 keys
+// c*16 .. c*16+15, in the key order of the probability operand (elements 0..3:
+// keys c*16 + grp*4 + 0..3, elements 4..7: keys c*16 + 8 + grp*4 + 0..3).
+// Each half is one transposing read: the 16 lanes of a group fetch 8 bytes of
+// 4 key rows and the hardware redistributes them so lane i receives dim i of
+// all four keys.
+template <int D>
+__device__ __forceinline__ u32x4_t vt_operand(const uint8_t *vb, int vofs, int c) {
+    constexpr int kRow = TileLayout<D>::kRow;
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4_t *)(vb + vofs + c * 16 * kRow));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4_t *)(vb + vofs + (c * 16 + 8) * kRow));
+    const u32x2_t l2 = __builtin_bit_cast(u32x2_t, lo), h2 = __builtin_bit_cast(u32x2_t, hi);
+    return __builtin_shufflevector(l2, h2, 0, 1, 2, 3);
 }
 
-// O^T += V^T P^T for one tile; each A operand is one 128-bit read of the
-// transposed V tile, issued RF_ATTN_V_LEAD operands ahead.
-template <int D, int kNB, int kVRow>
-__device__ __forceinline__ void pv_tile(const uint16_t *vb, const u32x4_t (&pw)[2 * kNB],
-                                        f32x16_t (&oacc)[D / 32], int col, int grp) {
+// O^T += V^T P^T for one tile; operands are read RF_ATTN_V_LEAD ahead.
+template <int D, int kNB>
+__device__ __forceinline__ void pv_tile(const uint8_t *vb, const int (&vofs)[D / 32],
+                                        const u32x4_t (&pw)[2 * kNB], f32x16_t (&oacc)[D / 32]) {
     constexpr int kNF = 2 * kNB * (D / 32);
     constexpr int kLead = RF_ATTN_V_LEAD < kNF ? RF_ATTN_V_LEAD : kNF;
     u32x4_t ring[kLead];
     auto rd = [&](int i) {
         const int c = i / (D / 32), db = i % (D / 32);
-        return *reinterpret_cast<const u32x4_t *>(&vb[(db * 32 + col) * kVRow + c * 16 + grp * 8]);
+        return vt_operand<D>(vb, vofs[db], c);
     };
 #pragma unroll
     for (int i = 0; i < kLead; ++i) ring[i] = rd(i);
@@ -190,45 +234,42 @@ __device__ __forceinline__ void pv_tile(const uint16_t *vb, const u32x4_t (&pw)[
                                                            oacc[db], 0, 0, 0);
         if (i + kLead < kNF) ring[i % kLead] = rd(i + kLead);
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, kLead, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * kLead, 0);
 #pragma unroll
     for (int i = 0; i < kNF - kLead; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
 }
 
-// Per-tile pipeline with double-buffered LDS and one barrier per tile:
-//   global loads of tile t+1 -> registers   (in flight during the math)
-//   math on LDS buffer t%2
-//   registers -> LDS buffer (t+1)%2          (last read during tile t-1)
-//   barrier
-// kBuf: K/V staging through raw buffer loads whose resource is rebased per
-// tile in scalar registers, so the hardware range check zero-fills keys >= S
-// and no per-tile vector address arithmetic is needed (tensors below 2 GiB).
-template <int D, bool kBuf>
+// Per-tile pipeline, double-buffered LDS, one barrier per tile:
+//   issue the global->LDS loads of tile t+1 into the buffer tile t-1 used
+//   math on tile t
+//   wait for this wave's loads, barrier (tile t+1 visible, tile t released)
+// The loads go through raw buffer resources rebased per tile in scalar
+// registers; the hardware range check zero-fills keys >= S. The loop is
+// unrolled by two so every LDS access names its buffer statically.
+template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnKArgs a) {
-    constexpr int kKRow = D + kKPad;                    // bf16 elements per K row
-    constexpr int kVRow = kBc + kVPad;                  // bf16 elements per V^T row
-    constexpr int kKTotal = kBc * D / 8;                // 16-byte K chunks per tile
-    constexpr int kVTotal = (kBc / 2) * (D / 8);        // (2 keys x 8 dims) V chunks per tile
-    constexpr int kKChunks = (kKTotal + kThreads - 1) / kThreads;
-    constexpr int kVChunks = (kVTotal + kThreads - 1) / kThreads;
+    using L = TileLayout<D>;
     constexpr int kNB = kBc / 32;                       // 32-key score blocks per tile
-    constexpr int kKBufs = 2;                           // K tile buffers (see the loop below)
-    constexpr int kVBufs = 2;                           // V tile buffers
+    constexpr int kLoadsPerWave = L::kLoads / kWaves;
+    static_assert(L::kLoads % kWaves == 0, "tile loads must split evenly over the waves");
 
-    __shared__ __attribute__((aligned(16))) uint16_t ks[kKBufs][kBc * kKRow];
-    __shared__ __attribute__((aligned(16))) uint16_t vt[kVBufs][D * kVRow];
+    __shared__ __attribute__((aligned(1024))) uint8_t k0[L::kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t k1[L::kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v0[L::kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v1[L::kTileBytes];
 
     const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
     if (tile >= a.total_tiles) return;
     const int head = tile / a.n_qtiles;
     const int qt = tile - head * a.n_qtiles;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int col = lane & 31, grp = lane >> 5;
     const int64_t rs = static_cast<int64_t>(a.heads) * D;   // token stride in elements
 
@@ -246,6 +287,28 @@ void attn_bf16_kernel(const AttnKArgs a) {
         for (int kk = 0; kk < D / 16; ++kk) qf[kk] = u32x4_t{0u, 0u, 0u, 0u};
     }
 
+    // ---- per-lane offsets, fixed for the whole loop ----
+    // global byte offsets (from the tile's first key) of this lane's 16 bytes in each load
+    int kgo[kLoadsPerWave], vgo[kLoadsPerWave];
+#pragma unroll
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+        const int key = (wave * kLoadsPerWave + i) * L::kRowsPerLoad + lane / L::kSlots;
+        const int slot = lane % L::kSlots;
+        kgo[i] = static_cast<int>(key * rs * 2) + (slot ^ L::kswz(key)) * 16;
+        vgo[i] = static_cast<int>(key * rs * 2) + (slot ^ L::vswz(key)) * 16;
+    }
+    // LDS byte offsets of the K fragment (block 0, step kk) and of the V^T operand halves
+    int kofs[D / 16], vofs[D / 32];
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) kofs[kk] = col * L::kRow + (((2 * kk) ^ grp ^ L::kswz(col)) * 16);
+    {
+        const int g16 = (lane >> 4) & 1, j = lane & 15;
+        const int rr = grp * 4 + j / 4;   // key row within each 8-key half of a 16-key group
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+            vofs[db] = rr * L::kRow + (((2 * db + g16) ^ (L::vswz(rr) / 2)) * 32) + 8 * (j % 4);
+    }
+
     f32x16_t oacc[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -260,107 +323,33 @@ void attn_bf16_kernel(const AttnKArgs a) {
 
     const uint16_t *kbase = a.k + static_cast<int64_t>(head) * D;
     const uint16_t *vbase = a.v + static_cast<int64_t>(head) * D;
-    const u32x4_t zero4 = {0u, 0u, 0u, 0u};
     // bytes from a head's first element to one past the last element it owns
     const int64_t head_bytes = ((a.S - 1) * rs + D) * 2;
 
-    u32x4_t kreg[kKChunks], vreg0[kVChunks], vreg1[kVChunks];
-
-    auto load_tile = [&](int64_t j0) {
-        if constexpr (kBuf) {
-            // scalar rebase: the resource starts at key j0, its range ends at the head's last key.
-            // The inputs are workgroup-uniform; readfirstlane states that to the compiler so the
-            // resource lives in scalar registers (no per-load uniformity loop).
-            const int64_t off = j0 * rs * 2;
-            const int32_t rec = __builtin_amdgcn_readfirstlane(static_cast<int32_t>(head_bytes - off));
-            const __amdgpu_buffer_rsrc_t kr =
-                __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + j0 * rs), 0, rec, kBufferWord3);
-            const __amdgpu_buffer_rsrc_t vr =
-                __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(vbase + j0 * rs), 0, rec, kBufferWord3);
+    auto issue = [&](int64_t j0, uint8_t *kdst, uint8_t *vdst) {
+        // The resources start at key j0; their range ends at the head's last key (clamped to
+        // 2^31 - 1: a tile never reaches that far past its first key).
+        const int64_t left = head_bytes - j0 * rs * 2;
+        const int32_t rec = __builtin_amdgcn_readfirstlane(
+            static_cast<int32_t>(left < 0x7fffffffLL ? left : 0x7fffffffLL));
+        const __amdgpu_buffer_rsrc_t kr =
+            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + j0 * rs), 0, rec, kBufferWord3);
+        const __amdgpu_buffer_rsrc_t vr =
+            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(vbase + j0 * rs), 0, rec, kBufferWord3);
 #pragma unroll
-            for (int i = 0; i < kKChunks; ++i) {
-                const int c = tid + i * kThreads;
-                if (kKTotal % kThreads != 0 && c >= kKTotal) break;
-                const int key = c / (D / 8), c8 = c % (D / 8);
-                kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(
-                    kr, static_cast<int32_t>((key * rs + c8 * 8) * 2), 0, 0);
-            }
-#pragma unroll
-            for (int i = 0; i < kVChunks; ++i) {
-                const int p = tid + i * kThreads;
-                if (kVTotal % kThreads != 0 && p >= kVTotal) break;
-                const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-                const int32_t o = static_cast<int32_t>((2 * kp * rs + c8 * 8) * 2);
-                vreg0[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, o, 0, 0);
-                vreg1[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, o + static_cast<int32_t>(rs * 2), 0, 0);
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < kKChunks; ++i) {
-                const int c = tid + i * kThreads;
-                if (kKTotal % kThreads != 0 && c >= kKTotal) break;
-                const int key = c / (D / 8), c8 = c % (D / 8);
-                const int64_t j = j0 + key;
-                kreg[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(kbase + j * rs + c8 * 8) : zero4;
-            }
-#pragma unroll
-            for (int i = 0; i < kVChunks; ++i) {
-                const int p = tid + i * kThreads;
-                if (kVTotal % kThreads != 0 && p >= kVTotal) break;
-                const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-                const int64_t j = j0 + 2 * kp;
-                vreg0[i] = j < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + j * rs + c8 * 8) : zero4;
-                vreg1[i] =
-                    j + 1 < a.S ? *reinterpret_cast<const u32x4_t *>(vbase + (j + 1) * rs + c8 * 8) : zero4;
-            }
-        }
-    };
-    auto store_tile = [&](int kbuf, int vbuf) {
-#pragma unroll
-        for (int i = 0; i < kKChunks; ++i) {
-            const int c = tid + i * kThreads;
-            if (kKTotal % kThreads != 0 && c >= kKTotal) break;
-            const int key = c / (D / 8), c8 = c % (D / 8);
-            *reinterpret_cast<u32x4_t *>(&ks[kbuf][key * kKRow + c8 * 8]) = kreg[i];
-        }
-#pragma unroll
-        for (int i = 0; i < kVChunks; ++i) {
-            const int p = tid + i * kThreads;
-            if (kVTotal % kThreads != 0 && p >= kVTotal) break;
-            const int kp = p % (kBc / 2), c8 = p / (kBc / 2);
-            uint32_t *dst = reinterpret_cast<uint32_t *>(&vt[vbuf][(c8 * 8) * kVRow + vt_column(2 * kp)]);
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                // word w holds dims 2w (low half) and 2w+1 (high half) of one key;
-                // the transposed row of a dim holds keys 2kp (low) and 2kp+1
-                // (high) side by side (vt_column keeps even/odd key pairs adjacent)
-                const uint32_t x0 = vreg0[i][w], x1 = vreg1[i][w];
-                dst[(2 * w) * (kVRow / 2)] = __builtin_amdgcn_perm(x1, x0, 0x05040100u);
-                dst[(2 * w + 1) * (kVRow / 2)] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
-            }
+        for (int i = 0; i < kLoadsPerWave; ++i) {
+            const int chunk = (wave * kLoadsPerWave + i) * 1024;
+            load_lds16(kr, (lds_void_t *)(kdst + chunk), kgo[i]);
+            load_lds16(vr, (lds_void_t *)(vdst + chunk), vgo[i]);
         }
     };
 
-    // Per-tile pipeline with double-buffered LDS and one barrier per tile:
-    //   global loads of tile t+1 -> registers   (in flight during the math)
-    //   math on LDS buffer t%2
-    //   registers -> LDS buffer (t+1)%2          (last read during tile t-1)
-    //   barrier
-    const int64_t ntiles = (a.S + kBc - 1) / kBc;
     const float sl2 = a.scale_log2;
-    load_tile(0);
-    store_tile(0, 0);
-    __syncthreads();
-    for (int64_t t = 0; t < ntiles; ++t) {
-        const int buf = static_cast<int>(t & 1);
-        if (t + 1 < ntiles) load_tile((t + 1) * kBc);   // in flight during this tile's math
-
+    auto compute = [&](int64_t j0, const uint8_t *kb, const uint8_t *vb) {
         // ---- S^T = K Q^T : 32-key blocks ----
         f32x16_t sacc[kNB];
-        scores_tile<D, kNB, kKRow>(ks[buf], qf, sacc, col, grp);
+        scores_tile<D, kNB>(kb, kofs, qf, sacc);
         // accumulator r of block b holds key b*32 + (r/4)*8 + grp*4 + r%4 for query `col`
-
-        const int64_t j0 = t * kBc;
         if (j0 + kBc > a.S) {
 #pragma unroll
             for (int b = 0; b < kNB; ++b)
@@ -408,10 +397,24 @@ void attn_bf16_kernel(const AttnKArgs a) {
         l_run += ls;
 
         // ---- O^T += V^T P^T ----
-        pv_tile<D, kNB, kVRow>(vt[buf], pw, oacc, col, grp);
-
-        if (t + 1 < ntiles) store_tile(buf ^ 1, buf ^ 1);
+        pv_tile<D, kNB>(vb, vofs, pw, oacc);
+    };
+    auto tile_done = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's loads have reached LDS
         __syncthreads();
+    };
+
+    const int64_t ntiles = (a.S + kBc - 1) / kBc;
+    issue(0, k0, v0);
+    tile_done();
+    for (int64_t t = 0; t < ntiles; t += 2) {
+        if (t + 1 < ntiles) issue((t + 1) * kBc, k1, v1);
+        compute(t * kBc, k0, v0);
+        tile_done();
+        if (t + 1 >= ntiles) break;
+        if (t + 2 < ntiles) issue((t + 2) * kBc, k0, v0);
+        compute((t + 1) * kBc, k1, v1);
+        tile_done();
     }
 
     // ---- epilogue: normalise, round to bf16, store the compact row ----
@@ -541,21 +544,16 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         const int64_t total = nq * p.heads;
         const int64_t per_xcd = (total + kXcds - 1) / kXcds;
         if (total > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
+        // per-lane load offsets inside a tile are 32-bit: kBc token rows must span < 2 GiB
+        if (static_cast<int64_t>(p.heads) * p.head_dim * 2 * kBc >= 0x7fffffffLL) return hipErrorInvalidConfiguration;
         a.n_qtiles = static_cast<int32_t>(nq);
         a.total_tiles = static_cast<int32_t>(total);
         a.per_xcd = static_cast<int32_t>(per_xcd);
         a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(p.head_dim)));
         for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
         const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds)), block(kThreads);
-        // buffer addressing covers a head's keys with 32-bit byte offsets
-        const bool buf = p.S * p.heads * p.head_dim * 2 < 0x7fffffffLL;
-        if (p.head_dim == 128) {
-            if (buf) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, stream, a);
-        } else {
-            if (buf) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, stream, a);
-        }
+        if (p.head_dim == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, stream, a);
+        else hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, stream, a);
         return hipGetLastError();
     }
     AttnF32Args a{};
