@@ -11,8 +11,8 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kThreads = 1024;   // one 16-byte vector per thread
+constexpr int kUnroll = 1;
 
 struct CopyKArgs {
     const u32x4 *src;

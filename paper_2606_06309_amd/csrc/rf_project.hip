@@ -6,14 +6,19 @@
 // Bandwidth-bound elementwise work: no matrix cores, no LDS. A workgroup
 // covers one contiguous chunk of one (b, c, f) plane, so alpha and the
 // keyframe flag are workgroup-uniform (scalar registers) and every access is
-// a coalesced 128-bit load or store.
+// a coalesced 128-bit streaming load or store.
 #include "rf_internal.h"
 
 namespace rf {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+// 512 threads x 2 vectors per workgroup and streaming (nontemporal) 16-byte
+// accesses: each byte is touched once, so nothing is kept in the caches.
+constexpr int kThreads = 512;
+constexpr int kUnroll = 2;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4_t ld16(const u32x4_t *p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st16(u32x4_t *p, u32x4_t v) { __builtin_nontemporal_store(v, p); }
 
 struct ProjKArgs {
     const void *lat;
@@ -56,37 +61,37 @@ __global__ __launch_bounds__(kThreads) void project_vec_kernel(const ProjKArgs a
     if (key && a.skip_keyframes) return;
 
     const int64_t in_plane = (c * a.T + f) * a.plane;
-    const uint4 *s0 = reinterpret_cast<const uint4 *>(
+    const u32x4_t *s0 = reinterpret_cast<const u32x4_t *>(
         static_cast<const char *>(a.lat) + (b * 2 * a.ctp + in_plane) * (kBf16 ? 2 : 4));
-    const uint4 *s1 = reinterpret_cast<const uint4 *>(
+    const u32x4_t *s1 = reinterpret_cast<const u32x4_t *>(
         static_cast<const char *>(a.lat) + ((b * 2 + 1) * a.ctp + in_plane) * (kBf16 ? 2 : 4));
-    uint4 *o = reinterpret_cast<uint4 *>(
+    u32x4_t *o = reinterpret_cast<u32x4_t *>(
         static_cast<char *>(a.out) + (b * a.ctp + in_plane) * (kBf16 ? 2 : 4));
     const int64_t nvec = a.plane / kPer;
     const int64_t base = static_cast<int64_t>(chunk) * kThreads * kUnroll + threadIdx.x;
 
     if (key) {  // keyframe: current state passes through
-        uint4 r[kUnroll];
+        u32x4_t r[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int64_t i = base + u * kThreads;
-            if (i < nvec) r[u] = s1[i];
+            if (i < nvec) r[u] = ld16(s1 + i);
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int64_t i = base + u * kThreads;
-            if (i < nvec) o[i] = r[u];
+            if (i < nvec) st16(o + i, r[u]);
         }
         return;
     }
 
-    uint4 x0[kUnroll], x1[kUnroll];
+    u32x4_t x0[kUnroll], x1[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
         const int64_t i = base + u * kThreads;
         if (i < nvec) {
-            x0[u] = s0[i];
-            x1[u] = s1[i];
+            x0[u] = ld16(s0 + i);
+            x1[u] = ld16(s1 + i);
         }
     }
     const float al = a.alpha, oma = a.one_minus_alpha;
@@ -109,7 +114,7 @@ __global__ __launch_bounds__(kThreads) void project_vec_kernel(const ProjKArgs a
                 r[e] = __float_as_uint(lerp3(__uint_as_float(w0[e]), __uint_as_float(w1[e]), al, oma));
             }
         }
-        o[i] = make_uint4(r[0], r[1], r[2], r[3]);
+        st16(o + i, u32x4_t{r[0], r[1], r[2], r[3]});
     }
 }
 
