@@ -26,8 +26,12 @@
 //    instructions), double-buffered so the next tile streams in while the
 //    current one is computed; the buffer range check zero-fills keys >= S and
 //    the last tile masks their scores.
-//  * Online softmax in the log2 domain with fp32 state; P is rounded to bf16
-//    for the matrix cores and the row sum adds those same rounded values.
+//  * Online softmax in the log2 domain with fp32 state, taken against a
+//    reference that is a past row maximum: the row maximum of a tile is only
+//    computed when the tile's row sum shows that a probability outgrew the
+//    reference (first tile, or a jump by a factor of ~256), so the common tile
+//    costs no max reduction. P is rounded to bf16 for the matrix cores and the
+//    row sum adds those same rounded values.
 //  * Workgroup ids are mapped XCD-aware: consecutive ids go round-robin to the
 //    8 XCDs, so tile = (id % 8) * per_xcd + id / 8 gives each XCD a contiguous,
 //    head-major range of tiles and the workgroups resident on one XCD stream
@@ -48,17 +52,17 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // instruction that consumes them.
 
 // Tunables (compile-time): waves per workgroup (each owns 32 query rows), keys
-// per LDS tile, the log2-domain slack before the running max is rebased (0:
-// the reference is always the exact running max, so the largest probability
-// is exactly 1), and how many LDS fragments the matrix core reads ahead.
+// per LDS tile, the largest row partial sum of a tile accepted before the
+// softmax reference is rebased (so every probability stays below it), and how
+// many LDS fragments the matrix core reads ahead.
 #ifndef RF_ATTN_WAVES
 #define RF_ATTN_WAVES 8
 #endif
 #ifndef RF_ATTN_BC
 #define RF_ATTN_BC 64
 #endif
-#ifndef RF_ATTN_RESCALE_SLACK
-#define RF_ATTN_RESCALE_SLACK 0.0f
+#ifndef RF_ATTN_REBASE_BOUND
+#define RF_ATTN_REBASE_BOUND 256.0f
 #endif
 #ifndef RF_ATTN_K_LEAD
 #define RF_ATTN_K_LEAD 4
@@ -72,6 +76,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
 constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
 constexpr int kXcds = 8;
+constexpr float kRebaseBound = RF_ATTN_REBASE_BOUND;   // largest tile row sum kept without a rebase
 static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
 
 struct AttnKArgs {
@@ -314,10 +319,8 @@ void attn_bf16_kernel(const AttnKArgs a) {
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
-    // m_run: reference max (log2 domain) the probabilities are taken against.
-    // It is rebased when the running max exceeds it by more than the slack, so
-    // p <= 2^slack; the final O / l does not depend on the reference. The
-    // accumulators are rescaled only on tiles where some lane rebased.
+    // m_run: reference max (log2 domain) the probabilities are taken against
+    // (a past row maximum; see the softmax below).
     float m_run = -__builtin_huge_valf();
     float l_run = 0.0f;   // this lane's partial row sum
 
@@ -360,40 +363,52 @@ void attn_bf16_kernel(const AttnKArgs a) {
                 }
         }
 
-        // ---- online softmax (log2 domain) ----
-        float mx = -__builtin_huge_valf();
+        // ---- online softmax (log2 domain), reference max moved only when needed ----
+        // p = exp2(s * scale - m_run) against the current reference m_run. The
+        // reference is a past row maximum, so p may exceed 1; that is harmless (O / l
+        // does not depend on the reference and floating-point relative precision does
+        // not depend on scale) until p grows large. The row sum bounds every p of the
+        // tile, so a row whose tile sum exceeds kRebaseBound takes the exact
+        // path: this tile's row maximum becomes the reference, O and l are
+        // rescaled and P is recomputed. The first tile (m_run = -inf gives
+        // p = inf) always takes it; afterwards it is rare.
+        u32x4_t pw[2 * kNB];
+        auto probs = [&]() {
+            // probabilities, packed as the B operand of O^T = V^T P^T:
+            // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2.
+            // The row sum adds the bf16-rounded values the matrix core consumes.
+            float ls = 0.0f;
 #pragma unroll
-        for (int b = 0; b < kNB; ++b)
+            for (int b = 0; b < kNB; ++b)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[b][r]);
-        mx = halves_max(mx) * sl2;
-        const bool rebase = mx > m_run + RF_ATTN_RESCALE_SLACK;
-        if (__builtin_amdgcn_ballot_w64(rebase)) {   // wave-uniform branch, rarer as the max settles
-            const float m_new = rebase ? mx : m_run;
-            const float corr = fast_exp2(m_run - m_new);
+                for (int r = 0; r < 16; r += 2) {
+                    const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_run));
+                    const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_run));
+                    const uint32_t word = pack_bf16x2(p0, p1);
+                    ls = add_bf16x2(word, ls);
+                    pw[b * 2 + r / 8][(r % 8) / 2] = word;
+                }
+            return ls;
+        };
+        float ls = probs();
+        // decided per query row (its two lanes agree), so a row's result depends on
+        // its own scores only, whichever rows share the wave
+        if (!(halves_sum(ls) <= kRebaseBound)) {   // rare; both lanes of a row take it
+            float mx = -__builtin_huge_valf();
+#pragma unroll
+            for (int b = 0; b < kNB; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[b][r]);
+            const float m_new = fmaxf(m_run, halves_max(mx) * sl2);
+            const float corr = fast_exp2(m_run - m_new);   // 0 on the first tile
             m_run = m_new;
             l_run *= corr;
 #pragma unroll
             for (int db = 0; db < D / 32; ++db)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) oacc[db][r] *= corr;
+            ls = probs();
         }
-
-        // probabilities, packed as the B operand of O^T = V^T P^T:
-        // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2.
-        // The row sum adds the bf16-rounded values the matrix core consumes.
-        u32x4_t pw[2 * kNB];
-        float ls = 0.0f;
-#pragma unroll
-        for (int b = 0; b < kNB; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; r += 2) {
-                const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_run));
-                const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_run));
-                const uint32_t word = pack_bf16x2(p0, p1);
-                ls = add_bf16x2(word, ls);
-                pw[b * 2 + r / 8][(r % 8) / 2] = word;
-            }
         l_run += ls;
 
         // ---- O^T += V^T P^T ----
