@@ -60,15 +60,19 @@ def test_ragged_multi_tile(d, dtype):
 
 @pytest.mark.parametrize("d", [64, 128])
 def test_sharp_softmax(d):
-    # Q scaled x2: logit std ~ 2, the running max grows across key tiles
+    """Q, K and V scaled x2: logit std ~ 4, the running max grows across key
+    tiles, and outputs reach |O| ~ 8, where rounding the exact result to bf16
+    alone is off by up to 2^-9 * 8 ~ 0.016; the bf16 bounds are applied to
+    O / max(1, max|O|)."""
     w = workloads.custom(6, 12, 15, 2, d, (0, 3, 5), dtype="bf16", seed=22)
     got, ref, _ = _run_case(w, scale=2.0)
-    assert_parity(got, ref, "bf16", "sharp")
+    s = max(1.0, float(np.abs(ref).max()))
+    assert_parity(got / s, ref / s, "bf16", "sharp (scaled)")
 
 
 @pytest.mark.parametrize("d", [64, 128])
 def test_peaked_softmax_relative(d):
-    """Q scaled x4 (logit std ~ 4): a few keys dominate, so outputs are O(1)
+    """Q, K and V scaled x4 (logit std ~ 16): a few keys dominate, so outputs are O(1)
     and bf16 rounding of P and of the output (unit roundoff 2^-8) produces
     errors proportional to |O|. The bf16 bounds are applied to O / max|O|."""
     w = workloads.custom(6, 9, 15, 2, d, (0, 3, 5), dtype="bf16", seed=22)
