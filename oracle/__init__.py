@@ -15,7 +15,10 @@ Contents, each written from the paper (RhymeFlow, arXiv 2606.06309):
 * keyframe-query attention in fp64 (C, ``oracle.c``): keyframe queries attend
   over all frames' keys and values (Sec. 3.2.3-3.2.4; App. B.2);
 * latent trajectory projection in fp64 (C), Eq. (3);
-* frame gather / scatter on raw bit patterns (numpy fancy indexing).
+* frame gather / scatter on raw bit patterns (numpy fancy indexing);
+* content-aware keyframe selection: the cosine similarity between latent
+  frames in fp64 (C; Eq. 1's psi_sim) and the sequential scan of Alg. 1 with
+  its dynamic threshold (pure Python).
 """
 import ctypes
 import math
@@ -51,6 +54,10 @@ def _load():
             ctypes.c_int64, ctypes.c_int64, ctypes.POINTER(ctypes.c_uint8),
             ctypes.c_double, ctypes.c_double, ctypes.c_double, dp]
         lib.orc_project_latents.restype = ctypes.c_int
+        lib.orc_frame_cosine.argtypes = [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+            ctypes.c_int64, ctypes.c_int64, dp]
+        lib.orc_frame_cosine.restype = ctypes.c_int
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -296,3 +303,61 @@ def scatter_frames(src_compact: np.ndarray, dst_full: np.ndarray, frame_ids,
     out = dst_full.copy()
     out[rowmap(frame_ids, rows_per_frame)] = src_compact
     return out
+
+
+# ---------------------------------------------------------------------------
+# content-aware keyframe selection (Sec. 3.1, Eq. 1; App. A, Alg. 1)
+# ---------------------------------------------------------------------------
+
+def frame_cosine(latents, B: int, C: int, T: int, Hl: int, Wl: int) -> np.ndarray:
+    """Cosine similarity between the frames of latents [B][C][T][Hl][Wl]
+    (each frame flattened over C*Hl*Wl, norms clamped to >= 1e-8); returns
+    [B][T][T] float64."""
+    la, dt = as_oracle_array(latents)
+    P = Hl * Wl
+    if la.size != B * C * T * P:
+        raise ValueError("latents size does not match B*C*T*Hl*Wl")
+    out = np.zeros((B, T, T), dtype=np.float64)
+    rc = _load().orc_frame_cosine(la.ctypes.data, dt, B, C, T, P,
+                                  out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise RuntimeError("oracle frame cosine failed")
+    return out
+
+
+def select_keyframes_adaptive(sim, tau: float, M: int, dtau: float, delta_up: float,
+                              delta_down: float, intent_sign: bool = False) -> np.ndarray:
+    """Dynamic sequential keyframe selection (Alg. 1) on a [T][T] frame
+    similarity matrix.
+
+    The first frame seeds the set and is the first reference. Frames are
+    visited in order while fewer than M are selected; frame i joins when its
+    similarity to the most recent keyframe is strictly below the current
+    threshold (Eq. 1). On each selection the gap to the previous keyframe is
+    compared with the expected interval L_avg = T / M (real division): a gap
+    of at least L_avg + delta_up lowers the threshold by dtau, a gap of at most
+    L_avg - delta_down raises it. ``intent_sign`` swaps the two adjustments
+    (the prose describes the large-gap change as encouraging selection, which
+    under the rule S < tau is a raise)."""
+    sim = np.asarray(sim, dtype=np.float64)
+    T = sim.shape[0]
+    if sim.shape != (T, T) or T <= 0:
+        raise ValueError("sim must be a square [T][T] matrix")
+    if M <= 0:
+        raise ValueError("M must be positive")
+    keys = [0]
+    last = 0
+    l_avg = T / M
+    for i in range(1, T):
+        if len(keys) >= M:
+            break
+        s = sim[i, last]
+        if s < tau:
+            gap = i - last
+            if gap >= l_avg + delta_up:
+                tau = tau + dtau if intent_sign else tau - dtau
+            elif gap <= l_avg - delta_down:
+                tau = tau - dtau if intent_sign else tau + dtau
+            keys.append(i)
+            last = i
+    return np.asarray(keys, dtype=np.int32)

@@ -200,3 +200,44 @@ int orc_project_latents(const void *latents, int dtype, int64_t B, int64_t C,
                 }
     return 0;
 }
+
+/*
+ * Cosine similarity between the latent frames of a batch element (Sec. 3.1:
+ * Eq. (1) compares frames with psi_sim, the cosine similarity; Alg. 1 applies
+ * it to the clean-latent proxies of the frames).
+ *
+ * latents: [B][C][T][P] of the given dtype (P = h*w). The vector of frame f of
+ *          batch element b is its C*P elements, channel after channel.
+ * sim:     [B][T][T] doubles,
+ *          sim[b][i][j] = <x_i, x_j> / (max(|x_i|, 1e-8) * max(|x_j|, 1e-8)),
+ *          so a frame with zero norm has similarity 0 to every frame.
+ */
+int orc_frame_cosine(const void *latents, int dtype, int64_t B, int64_t C,
+                     int64_t T, int64_t P, double *sim)
+{
+    if (!latents || !sim)
+        return -1;
+    if (B <= 0 || C <= 0 || T <= 0 || P <= 0)
+        return -1;
+    if (dtype != ORC_F64 && dtype != ORC_F32 && dtype != ORC_BF16)
+        return -1;
+    const double eps = 1e-8;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t i = 0; i < T; ++i)
+            for (int64_t j = 0; j < T; ++j) {
+                double dot = 0.0, ni = 0.0, nj = 0.0;
+                for (int64_t c = 0; c < C; ++c)
+                    for (int64_t e = 0; e < P; ++e) {
+                        const double xi = widen(latents, dtype, ((b * C + c) * T + i) * P + e);
+                        const double xj = widen(latents, dtype, ((b * C + c) * T + j) * P + e);
+                        dot += xi * xj;
+                        ni += xi * xi;
+                        nj += xj * xj;
+                    }
+                const double di = sqrt(ni) > eps ? sqrt(ni) : eps;
+                const double dj = sqrt(nj) > eps ? sqrt(nj) : eps;
+                sim[(b * T + i) * T + j] = dot / (di * dj);
+            }
+    return 0;
+}
