@@ -55,6 +55,8 @@ typedef enum { RF_BF16 = 0, RF_F32 = 1 } rf_dtype;
 
 /* Flags of rf_select_keyframes. */
 #define RF_SEL_NO_FORCE_FIRST 1u
+/* Flags of rf_select_keyframes_adaptive. */
+#define RF_SEL_INTENT_SIGN 1u
 
 /* Name of a status code (static string). */
 const char *rf_status_string(int status);
@@ -180,6 +182,63 @@ int rf_gather_frames(const void *src_full, void *dst_compact,
 int rf_scatter_frames(const void *src_compact, void *dst_full,
                       const int32_t *frame_ids, int32_t M, int32_t T,
                       int64_t rows_per_frame, int64_t row_bytes, void *stream);
+
+/*
+ * Cosine similarity between latent frames (content-aware keyframe selection,
+ * Sec. 3.1: Eq. (1) compares a frame with the most recent keyframe by cosine
+ * similarity; Alg. 1 computes it on the frames' clean-latent proxies).
+ *
+ * latents: device, [B][C][T][H][W] contiguous, RF_F32 or RF_BF16 (the proxies,
+ *          e.g. a single-step clean-latent prediction; supplied by the caller).
+ *          The vector of frame f of batch element b is its C*H*W elements.
+ * sim_out: device, [B][T][T] doubles:
+ *          sim[b][i][j] = <x_i, x_j> / (max(|x_i|, 1e-8) * max(|x_j|, 1e-8)),
+ *          products and sums in double precision (a frame with zero norm has
+ *          similarity 0 to every frame).
+ * workspace: device scratch of at least workspace_bytes bytes, as returned by
+ *          rf_frame_similarity_workspace for the same sizes; its contents are
+ *          overwritten and are meaningless afterwards. It must not overlap
+ *          latents or sim_out.
+ * T: 1..RF_MAX_FRAMES. latents and workspace 16-byte aligned, sim_out 8-byte.
+ * The result is deterministic (fixed-order reductions).
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0, overlap, workspace too small),
+ *         RF_ERR_RANGE (T), RF_ERR_UNSUPPORTED (dtype, alignment), RF_ERR_HIP.
+ */
+int rf_frame_similarity(const void *latents, double *sim_out, void *workspace,
+                        int64_t workspace_bytes, int32_t B, int32_t C, int32_t T,
+                        int32_t H, int32_t W, int32_t dtype, void *stream);
+
+/*
+ * Bytes of device workspace rf_frame_similarity needs for these sizes
+ * (host only). Errors: RF_ERR_INVALID_ARG, RF_ERR_RANGE (T).
+ */
+int rf_frame_similarity_workspace(int32_t B, int32_t C, int32_t T, int32_t H, int32_t W,
+                                  int64_t *bytes_out);
+
+/*
+ * Dynamic sequential keyframe selection (Alg. 1; Eq. 1) on a frame similarity
+ * matrix (host only; the decisions are integer).
+ *
+ * The first frame seeds the set and is the first reference. Frames i = 1..T-1
+ * are visited in order while fewer than M are selected; frame i joins when
+ * sim[i][last] < tau, with `last` the most recent keyframe (strict <). On each
+ * selection, the gap g = i - last is compared with L_avg = T / M (real
+ * division): g >= L_avg + delta_up lowers tau by dtau, g <= L_avg - delta_down
+ * raises it (Alg. 1 as printed). RF_SEL_INTENT_SIGN swaps the two adjustments
+ * (the prose calls the large-gap adjustment encouraging, which under the
+ * rule sim < tau is a raise).
+ *
+ * sim: host, [T][T] doubles, row-major (only sim[i][last] entries are read).
+ * T: 1..RF_MAX_FRAMES. M: 1..T. tau, dtau, delta_up, delta_down: finite.
+ * keyframe_ids_out: host, capacity T; *num_keyframes_out = selected count;
+ * keyframe_mask_out: host [T] or NULL.
+ * Errors: RF_ERR_INVALID_ARG (NULL, non-finite parameter, unknown flag),
+ *         RF_ERR_RANGE (T, M).
+ */
+int rf_select_keyframes_adaptive(const double *sim, int32_t T, double tau, int32_t M,
+                                 double dtau, double delta_up, double delta_down, uint32_t flags,
+                                 int32_t *keyframe_ids_out, int32_t *num_keyframes_out,
+                                 uint8_t *keyframe_mask_out);
 
 #ifdef __cplusplus
 }

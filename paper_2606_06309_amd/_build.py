@@ -17,7 +17,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librhymeflow.so")
 ARCH = "gfx950"
 
-SOURCES = ["rf_abi.cpp", "rf_attention.hip", "rf_project.hip", "rf_gather.hip"]
+SOURCES = ["rf_abi.cpp", "rf_attention.hip", "rf_project.hip", "rf_gather.hip", "rf_similarity.hip"]
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

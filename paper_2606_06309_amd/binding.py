@@ -24,6 +24,7 @@ RF_ERR_HIP = -4
 RF_BF16 = 0
 RF_F32 = 1
 RF_SEL_NO_FORCE_FIRST = 1
+RF_SEL_INTENT_SIGN = 1
 RF_MAX_FRAMES = 256
 
 EXPORTED = [
@@ -31,6 +32,7 @@ EXPORTED = [
     "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
     "rf_project_latents", "rf_keyframe_attention",
     "rf_gather_frames", "rf_scatter_frames",
+    "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
 ]
 
 
@@ -75,6 +77,14 @@ lib.rf_gather_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
 lib.rf_gather_frames.restype = ctypes.c_int
 lib.rf_scatter_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
 lib.rf_scatter_frames.restype = ctypes.c_int
+lib.rf_frame_similarity.argtypes = [_vp, _vp, _vp, _i64, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
+lib.rf_frame_similarity.restype = ctypes.c_int
+lib.rf_frame_similarity_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64)]
+lib.rf_frame_similarity_workspace.restype = ctypes.c_int
+lib.rf_select_keyframes_adaptive.argtypes = [_dp, _i32, ctypes.c_double, _i32, ctypes.c_double,
+                                             ctypes.c_double, ctypes.c_double, ctypes.c_uint32,
+                                             _i32p, _i32p, _u8p]
+lib.rf_select_keyframes_adaptive.restype = ctypes.c_int
 
 
 def _check(status: int):
@@ -140,6 +150,34 @@ def rf_keyframes_stride(T: int, k: int) -> np.ndarray:
     return out[:n.value].copy()
 
 
+def rf_select_keyframes_adaptive(sim, tau: float, M: int, dtau: float, delta_up: float,
+                                 delta_down: float, intent_sign: bool = False):
+    """Alg. 1's scan on a host [T][T] similarity matrix (numpy or a tensor,
+    copied to host). Returns (keyframe ids int32, mask uint8 [T])."""
+    if isinstance(sim, torch.Tensor):
+        sim = sim.detach().cpu().numpy()
+    a = np.ascontiguousarray(np.asarray(sim, dtype=np.float64))
+    if a.ndim != 2 or a.shape[0] != a.shape[1]:
+        raise ValueError("sim must be a square [T][T] matrix")
+    T = a.shape[0]
+    out = np.zeros(max(T, 1), dtype=np.int32)
+    mask = np.zeros(max(T, 1), dtype=np.uint8)
+    n = ctypes.c_int32(0)
+    flags = RF_SEL_INTENT_SIGN if intent_sign else 0
+    _check(lib.rf_select_keyframes_adaptive(a.ctypes.data_as(_dp), T, float(tau), M, float(dtau),
+                                            float(delta_up), float(delta_down), flags,
+                                            out.ctypes.data_as(_i32p), ctypes.byref(n),
+                                            mask.ctypes.data_as(_u8p)))
+    return out[:n.value].copy(), mask[:T].copy()
+
+
+def rf_frame_similarity_workspace(B: int, C: int, T: int, H: int, W: int) -> int:
+    """Bytes of device workspace rf_frame_similarity needs."""
+    n = _i64(0)
+    _check(lib.rf_frame_similarity_workspace(B, C, T, H, W, ctypes.byref(n)))
+    return int(n.value)
+
+
 def rf_keyframes_uniform(T: int, M: int) -> np.ndarray:
     out = np.zeros(max(M, 1), dtype=np.int32)
     n = ctypes.c_int32(0)
@@ -186,6 +224,25 @@ def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=Non
     _check(lib.rf_keyframe_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                      ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
                                      _stream(stream)))
+    return out
+
+
+def rf_frame_similarity(latents: torch.Tensor, out=None, workspace=None, stream=None):
+    """latents [B][C][T][H][W] -> cosine similarity [B][T][T] float64 (device).
+    The workspace (a device uint8 tensor) is allocated here if not given."""
+    if latents.dim() != 5:
+        raise ValueError("latents must be [B][C][T][H][W]")
+    B, C, T, H, W = latents.shape
+    if out is None:
+        out = torch.empty((B, T, T), dtype=torch.float64, device=latents.device)
+    if out.dtype != torch.float64 or out.numel() != B * T * T:
+        raise ValueError("out must be float64 [B][T][T]")
+    need = rf_frame_similarity_workspace(B, C, T, H, W)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=latents.device)
+    _check(lib.rf_frame_similarity(_dev(latents, "latents"), _dev(out, "out"),
+                                   _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                   B, C, T, H, W, _dtype_code(latents.dtype), _stream(stream)))
     return out
 
 

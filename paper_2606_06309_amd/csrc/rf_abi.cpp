@@ -269,4 +269,90 @@ int rf_scatter_frames(const void *src_compact, void *dst_full, const int32_t *fr
                       "rf_scatter_frames");
 }
 
+int rf_frame_similarity_workspace(int32_t B, int32_t C, int32_t T, int32_t H, int32_t W,
+                                  int64_t *bytes_out) {
+    const char *fn = "rf_frame_similarity_workspace";
+    if (!bytes_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    if (B <= 0 || C <= 0 || T <= 0 || H <= 0 || W <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (B=%d C=%d T=%d H=%d W=%d)",
+                    fn, B, C, T, H, W);
+    if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
+    const rf::SimGeometry g = rf::similarity_geometry(B, C, T, static_cast<int64_t>(H) * W);
+    if (static_cast<double>(B) * static_cast<double>(g.n_runs) * g.NBP * 128.0 > 4.0e18 ||
+        static_cast<double>(C) * H * W * T * B > 4.0e18)
+        return fail(RF_ERR_RANGE, "%s: workspace size overflows", fn);
+    *bytes_out = g.workspace_bytes;
+    return ok();
+}
+
+int rf_frame_similarity(const void *latents, double *sim_out, void *workspace,
+                        int64_t workspace_bytes, int32_t B, int32_t C, int32_t T, int32_t H,
+                        int32_t W, int32_t dtype, void *stream) {
+    const char *fn = "rf_frame_similarity";
+    if (!latents || !sim_out || !workspace) return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);
+    int64_t need = 0;
+    const int rc = rf_frame_similarity_workspace(B, C, T, H, W, &need);
+    if (rc != RF_OK) return rc;
+    if (dtype != RF_F32 && dtype != RF_BF16)
+        return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (!aligned16(latents) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(sim_out) & 7u))
+        return fail(RF_ERR_UNSUPPORTED, "%s: latents/workspace must be 16-byte and sim_out 8-byte aligned", fn);
+    if (workspace_bytes < need)
+        return fail(RF_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed", fn,
+                    static_cast<long long>(workspace_bytes), static_cast<long long>(need));
+    const int64_t plane = static_cast<int64_t>(H) * W;
+    const int64_t lat_bytes = static_cast<int64_t>(B) * C * T * plane * (dtype == RF_F32 ? 4 : 2);
+    const int64_t sim_bytes = static_cast<int64_t>(B) * T * T * 8;
+    if (overlaps(sim_out, sim_bytes, latents, lat_bytes) || overlaps(sim_out, sim_bytes, workspace, need) ||
+        overlaps(workspace, need, latents, lat_bytes))
+        return fail(RF_ERR_INVALID_ARG, "%s: latents, sim_out and workspace must not overlap", fn);
+    rf::SimParams p{};
+    p.latents = latents;
+    p.sim = sim_out;
+    p.workspace = static_cast<double *>(workspace);
+    p.plane = plane;
+    p.B = B;
+    p.C = C;
+    p.T = T;
+    p.dtype = dtype;
+    return launched(rf::launch_similarity(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_select_keyframes_adaptive(const double *sim, int32_t T, double tau, int32_t M, double dtau,
+                                 double delta_up, double delta_down, uint32_t flags,
+                                 int32_t *keyframe_ids_out, int32_t *num_keyframes_out,
+                                 uint8_t *keyframe_mask_out) {
+    const char *fn = "rf_select_keyframes_adaptive";
+    if (!sim || !keyframe_ids_out || !num_keyframes_out)
+        return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);
+    if (T <= 0 || T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d outside 1..%d", fn, T, RF_MAX_FRAMES);
+    if (M <= 0 || M > T) return fail(RF_ERR_RANGE, "%s: M = %d outside 1..%d", fn, M, T);
+    if (!isfinite(tau) || !isfinite(dtau) || !isfinite(delta_up) || !isfinite(delta_down))
+        return fail(RF_ERR_INVALID_ARG, "%s: tau, dtau, delta_up and delta_down must be finite", fn);
+    if (flags & ~RF_SEL_INTENT_SIGN) return fail(RF_ERR_INVALID_ARG, "%s: unknown flags 0x%x", fn, flags);
+    const bool intent = (flags & RF_SEL_INTENT_SIGN) != 0;
+    // Alg. 1: the first frame seeds the set; expected interval L_avg = T / M.
+    const double l_avg = static_cast<double>(T) / static_cast<double>(M);
+    int32_t n = 0, last = 0;
+    keyframe_ids_out[n++] = 0;
+    for (int32_t i = 1; i < T && n < M; ++i) {
+        // Eq. (1): compare with the most recent keyframe, strictly below the threshold
+        if (sim[static_cast<int64_t>(i) * T + last] < tau) {
+            const double gap = static_cast<double>(i - last);
+            if (gap >= l_avg + delta_up)
+                tau = intent ? tau + dtau : tau - dtau;
+            else if (gap <= l_avg - delta_down)
+                tau = intent ? tau - dtau : tau + dtau;
+            keyframe_ids_out[n++] = i;
+            last = i;
+        }
+    }
+    *num_keyframes_out = n;
+    if (keyframe_mask_out) {
+        for (int32_t f = 0; f < T; ++f) keyframe_mask_out[f] = 0;
+        for (int32_t m = 0; m < n; ++m) keyframe_mask_out[keyframe_ids_out[m]] = 1;
+    }
+    return ok();
+}
+
 }  // extern "C"

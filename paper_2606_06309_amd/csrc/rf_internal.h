@@ -53,4 +53,31 @@ struct FrameCopyParams {
 
 hipError_t launch_frame_copy(const FrameCopyParams &p, hipStream_t stream);
 
+// Frame cosine similarity: blocking of the frame Gram matrix over feature
+// chunks (shared by the workspace query and the launcher).
+struct SimGeometry {
+    int32_t Tp;               // frames rounded up to a multiple of 4
+    int32_t NB;               // 4-frame blocks
+    int32_t NBP;              // block pairs (bi <= bj)
+    int32_t L;                // feature elements per chunk
+    int64_t chunks_per_plane;
+    int64_t n_chunks;         // per batch element: C * chunks_per_plane
+    int64_t run;              // consecutive chunks one workgroup accumulates
+    int64_t n_runs;           // workgroups (partial Gram blocks) per batch element
+    int64_t workspace_bytes;  // B * n_runs * NBP * 16 doubles
+};
+
+SimGeometry similarity_geometry(int32_t B, int32_t C, int32_t T, int64_t plane);
+
+struct SimParams {
+    const void *latents;
+    double *sim;
+    double *workspace;
+    int64_t plane;            // H * W
+    int32_t B, C, T;
+    int32_t dtype;
+};
+
+hipError_t launch_similarity(const SimParams &p, hipStream_t stream);
+
 }  // namespace rf

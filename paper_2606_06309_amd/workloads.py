@@ -142,3 +142,19 @@ def sample_rows(w: Workload, per_head: int, tile: int = 128, seed: int = 1234):
         pool = np.setdiff1d(np.arange(Mq), np.array(rows))
         rows += rng.choice(pool, min(extra, pool.size), replace=False).tolist()
     return np.array(sorted(rows), dtype=np.int64)
+
+
+def make_scene_latents(B: int, C: int, T: int, H: int, W: int, cut_frames, noise: float = 0.3,
+                       seed: int = 7, device="cpu", dtype=torch.float32):
+    """Synthetic clean-latent proxies [B][C][T][H][W] with scene cuts: frames of
+    one scene share a random base and differ by independent noise of relative
+    size `noise`; a new scene (new base) starts at every listed cut frame."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    cuts = sorted(set(int(f) for f in cut_frames) | {0})
+    x = torch.empty((B, C, T, H, W), dtype=torch.float32, device=device)
+    for si, start in enumerate(cuts):
+        end = cuts[si + 1] if si + 1 < len(cuts) else T
+        base = torch.randn((B, C, 1, H, W), generator=g, device=device)
+        x[:, :, start:end] = base + noise * torch.randn((B, C, end - start, H, W), generator=g, device=device)
+    return x.to(dtype)

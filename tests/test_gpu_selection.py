@@ -1,0 +1,101 @@
+"""GPU parity of the frame cosine similarity (Eq. 1's psi_sim, Alg. 1) through
+the C ABI against the fp64 oracle, and content-aware keyframe selection end to
+end on synthetic scene-cut proxies."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_06309_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+rf = pytest.importorskip("paper_2606_06309_amd.binding")
+
+SIM_TOL = 1e-12   # products exact in double, sums in a different order than the oracle
+
+
+def _case(B, C, T, H, W, dtype=torch.float32, seed=0, scale=1.0):
+    print(f"[case] similarity B={B} C={C} T={T} H={H} W={W} dtype={dtype}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    x = (torch.randn((B, C, T, H, W), generator=g, device="cuda") * scale).to(dtype)
+    sim = rf.rf_frame_similarity(x)
+    torch.cuda.synchronize()
+    ref = oracle.frame_cosine(x.cpu(), B, C, T, H, W)
+    return x, sim.cpu().numpy(), ref
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 4, 5, 8, 8),          # one chunk per channel plane
+    (2, 3, 7, 17, 19),        # plane 323: ragged chunk tail; T not a multiple of 4
+    (1, 16, 21, 30, 52),      # the 480p latent grid
+    (1, 2, 1, 9, 9),          # a single frame
+    (1, 1, 256, 8, 8),        # the largest T (64-element chunks)
+    (1, 2, 66, 40, 40),       # more block pairs than threads in a workgroup
+])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_similarity_parity(shape, dtype):
+    _, sim, ref = _case(*shape, dtype=dtype)
+    assert np.all(np.isfinite(sim))
+    assert np.abs(sim - ref).max() <= SIM_TOL
+
+
+def test_similarity_long_workload_grid():
+    w = workloads.WORKLOADS["long"]
+    Hl, Wl = w.latent_hw
+    x = workloads.make_scene_latents(1, w.latent_c, w.T, Hl, Wl, (6, 12, 18, 22, 24, 30), device="cuda")
+    sim = rf.rf_frame_similarity(x)
+    torch.cuda.synchronize()
+    ref = oracle.frame_cosine(x.cpu(), 1, w.latent_c, w.T, Hl, Wl)
+    assert np.abs(sim.cpu().numpy() - ref).max() <= SIM_TOL
+
+
+def test_similarity_properties():
+    x, sim, _ = _case(2, 3, 9, 11, 13, seed=3)
+    s = sim
+    assert np.array_equal(s, np.transpose(s, (0, 2, 1)))          # symmetric bit for bit
+    assert np.all(np.abs(np.diagonal(s, axis1=1, axis2=2) - 1.0) <= 1e-14)
+    again = rf.rf_frame_similarity(x).cpu().numpy()
+    assert np.array_equal(s, again)                                 # deterministic
+
+
+def test_zero_frame_and_dirty_workspace():
+    B, C, T, H, W = 1, 2, 6, 10, 12
+    g = torch.Generator(device="cuda").manual_seed(4)
+    x = torch.randn((B, C, T, H, W), generator=g, device="cuda")
+    x[:, :, 3] = 0.0
+    need = rf.rf_frame_similarity_workspace(B, C, T, H, W)
+    ws = torch.full((need // 8,), float("nan"), dtype=torch.float64, device="cuda")
+    out = torch.full((B, T, T), float("nan"), dtype=torch.float64, device="cuda")
+    rf.rf_frame_similarity(x, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    s = out.cpu().numpy()[0]
+    assert np.all(s[3] == 0.0) and np.all(s[:, 3] == 0.0)
+    ref = oracle.frame_cosine(x.cpu(), B, C, T, H, W)[0]
+    assert np.abs(s - ref).max() <= SIM_TOL
+
+
+def test_scale_invariance():
+    # a power-of-two scale is exact in every format, so only rounding of the
+    # reductions may differ (in practice nothing does)
+    _, a, _ = _case(1, 3, 6, 9, 9, seed=5)
+    _, b, _ = _case(1, 3, 6, 9, 9, seed=5, scale=2.0 ** -10)
+    assert np.abs(a - b).max() <= 1e-14
+
+
+@pytest.mark.parametrize("intent", [False, True])
+def test_selection_end_to_end(intent):
+    """Similarity on the GPU, Alg. 1's scan in the library; equal to the
+    oracle's scan of the oracle's similarity on scene-cut proxies."""
+    w = workloads.WORKLOADS["long"]
+    Hl, Wl = w.latent_hw
+    cuts = (5, 9, 17, 26, 29)
+    x = workloads.make_scene_latents(1, w.latent_c, w.T, Hl, Wl, cuts, noise=0.5, device="cuda",
+                                     dtype=torch.bfloat16)
+    sim = rf.rf_frame_similarity(x)
+    torch.cuda.synchronize()
+    ids, mask = rf.rf_select_keyframes_adaptive(sim[0], 0.5, 8, 0.05, 2.0, 2.0, intent)
+    ref_sim = oracle.frame_cosine(x.cpu(), 1, w.latent_c, w.T, Hl, Wl)[0]
+    exp = oracle.select_keyframes_adaptive(ref_sim, 0.5, 8, 0.05, 2.0, 2.0, intent)
+    assert ids.tolist() == exp.tolist()
+    assert set(cuts) <= set(ids.tolist())      # every scene start is found
