@@ -40,6 +40,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--no-bandwidth", action="store_true")
+    ap.add_argument("--no-selection", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU work of the oracle baseline sample")
     return ap.parse_args()
@@ -111,8 +112,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}): "
-              "the keyframe-query attention path has no multi-GPU form in this build; "
-              "see DESIGN.md for how it would shard by head.", file=sys.stderr)
+              "the keyframe-query attention path is provided for a single GPU; across GPUs it "
+              "would shard by head, with no exchange between GPUs.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -211,11 +212,52 @@ def main():
     if not args.no_bandwidth:
         result["bandwidth"] = bandwidth(w, q, attn_out, full_out, args)
 
+    if not args.no_selection:
+        result["selection"] = selection(w, args)
+
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def selection(w, args):
+    """Content-aware keyframe selection (Sec. 3.1, Alg. 1) on synthetic
+    clean-latent proxies of the workload's latent grid with scene cuts: the
+    frame cosine similarity on the GPU (bytes = the proxies read once) and
+    Alg. 1's scan on the host."""
+    import torch
+    from paper_2606_06309_amd import binding as rf, workloads
+
+    Hl, Wl = w.latent_hw
+    cuts = tuple(range(5, w.T, 6))
+    x = workloads.make_scene_latents(1, w.latent_c, w.T, Hl, Wl, cuts, noise=0.5, device="cuda")
+    ws = torch.empty(rf.rf_frame_similarity_workspace(1, w.latent_c, w.T, Hl, Wl),
+                     dtype=torch.uint8, device="cuda")
+    sim = torch.empty((1, w.T, w.T), dtype=torch.float64, device="cuda")
+    for _ in range(3):
+        rf.rf_frame_similarity(x, out=sim, workspace=ws)
+    torch.cuda.synchronize()
+    n = max(5, args.steps)
+    ev = _events(n)
+    for a, b in ev:
+        a.record()
+        rf.rf_frame_similarity(x, out=sim, workspace=ws)
+        b.record()
+    torch.cuda.synchronize()
+    ms = _avg_ms(ev)
+    host = sim[0].cpu().numpy()
+    t0 = time.perf_counter()
+    ids, _ = rf.rf_select_keyframes_adaptive(host, 0.5, w.M, 0.05, 2.0, 2.0)
+    scan_us = (time.perf_counter() - t0) * 1e6
+    nbytes = x.numel() * x.element_size()
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(f"[bench] selection: similarity {ms * 1e3:.1f} us ({gbs:.0f} GB/s), scan {scan_us:.0f} us, "
+          f"keyframes {ids.tolist()}", file=sys.stderr, flush=True)
+    return {"similarity_avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
+            "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "scan_us": round(scan_us, 1),
+            "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
 
 
 def bandwidth(w, q, attn_out, full_out, args):
