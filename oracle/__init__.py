@@ -18,7 +18,12 @@ Contents, each written from the paper (RhymeFlow, arXiv 2606.06309):
 * frame gather / scatter on raw bit patterns (numpy fancy indexing);
 * content-aware keyframe selection: the cosine similarity between latent
   frames in fp64 (C; Eq. 1's psi_sim) and the sequential scan of Alg. 1 with
-  its dynamic threshold (pure Python).
+  its dynamic threshold (pure Python);
+* the per-layer rolling cache of App. B.2 (pure Python/numpy, fp64): two cached
+  post-attention hidden states per non-keyframe with their timesteps,
+  initialisation at the end of warm-up, shift-and-store at denoising steps,
+  the projection with the epsilon form of alpha at skipped steps, and the
+  key/value sequence in which the projected state is both key and value.
 """
 import ctypes
 import math
@@ -361,3 +366,78 @@ def select_keyframes_adaptive(sim, tau: float, M: int, dtau: float, delta_up: fl
             keys.append(i)
             last = i
     return np.asarray(keys, dtype=np.int32)
+
+
+# ---------------------------------------------------------------------------
+# rolling cache of post-attention hidden states (App. B.2)
+# ---------------------------------------------------------------------------
+
+HIDDEN_EPS = 1e-8
+
+
+def hidden_alpha(t_before: float, t_after: float, t_skip: float) -> float:
+    """alpha = (t_before - t_skip) / (t_before - t_after + eps), eps = 1e-8,
+    kept in [0, 1] (right after initialisation t_before = t_after, which makes
+    the quotient huge; clamped it selects the cached state, which both slots
+    hold then)."""
+    for t in (t_before, t_after, t_skip):
+        if not math.isfinite(t):
+            raise ValueError("timesteps must be finite")
+    a = (t_before - t_skip) / (t_before - t_after + HIDDEN_EPS)
+    return min(1.0, max(0.0, a))
+
+
+class RollingCache:
+    """The per-layer, per-frame cache of App. B.2 for one layer, written as the
+    appendix states it: each frame holds h_before and h_after (arrays of the
+    frame's hidden states) and the timesteps t_before >= t_after."""
+
+    def __init__(self):
+        self.h_before, self.h_after = {}, {}
+        self.t_before, self.t_after = {}, {}
+
+    def init(self, frames, h, t_w: float):
+        """End of warm-up: h_before = h_after = the attention output at t_w."""
+        for f in frames:
+            self.h_before[f] = np.array(h[f], dtype=np.float64)
+            self.h_after[f] = np.array(h[f], dtype=np.float64)
+            self.t_before[f] = self.t_after[f] = float(t_w)
+
+    def shift_and_store(self, frames, h_new, t_denoise: float):
+        """At a denoising (Rhythmic Point) step: h_before <- h_after,
+        t_before <- t_after, h_after <- the new attention output, t_after <- t."""
+        for f in frames:
+            self.h_before[f] = self.h_after[f]
+            self.t_before[f] = self.t_after[f]
+            self.h_after[f] = np.array(h_new[f], dtype=np.float64)
+            self.t_after[f] = float(t_denoise)
+
+    def project(self, f, t_skip: float) -> np.ndarray:
+        """h at a skipped step: (1 - alpha) h_before + alpha h_after."""
+        a = hidden_alpha(self.t_before[f], self.t_after[f], t_skip)
+        return (1.0 - a) * self.h_before[f] + a * self.h_after[f]
+
+
+def skip_step_kv(k, v, cache: RollingCache, nonkey_frames, t_skip: float, N: int):
+    """Keys and values over all frames at a skipped step: keyframes keep their
+    computed K and V; every listed non-keyframe contributes its projected hidden
+    state as both key and value (App. B.2). k, v: [T*N][heads][d] (any exact
+    dtype); returns float64 copies."""
+    K = as_oracle_f64(k)
+    V = as_oracle_f64(v)
+    shape = K.shape
+    K = K.reshape(-1, N, *shape[1:])
+    V = V.reshape(-1, N, *shape[1:])
+    for f in nonkey_frames:
+        h = cache.project(f, t_skip).reshape(N, *shape[1:])
+        K[f] = h
+        V[f] = h
+    return K.reshape(shape), V.reshape(shape)
+
+
+def as_oracle_f64(x) -> np.ndarray:
+    """float64 copy of a tensor's exact values (bf16 widened exactly)."""
+    a, dt = as_oracle_array(x)
+    if dt == BF16:
+        return bf16_bits_to_f64(a).reshape(a.shape)
+    return np.array(a, dtype=np.float64)
