@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--no-bandwidth", action="store_true")
     ap.add_argument("--no-selection", action="store_true")
+    ap.add_argument("--no-cache", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU work of the oracle baseline sample")
     return ap.parse_args()
@@ -215,6 +216,9 @@ def main():
     if not args.no_selection:
         result["selection"] = selection(w, args)
 
+    if not args.no_cache:
+        result["rolling_cache"] = rolling_cache(w, args)
+
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
@@ -258,6 +262,58 @@ def selection(w, args):
     return {"similarity_avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "scan_us": round(scan_us, 1),
             "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
+
+
+def rolling_cache(w, args):
+    """Rolling cache of App. B.2 at the workload's shape: every non-keyframe
+    cached (bf16 [N][heads*head_dim] states). Times the projection of the
+    cached frames into K and V at a skipped step and the shift-and-store copy
+    of a denoising step; both move well over the 256 MB Infinity Cache."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    nk = [f for f in range(w.T) if f not in w.keyframes]
+    D = w.heads * w.head_dim
+    el = torch.tensor([], dtype=w.torch_dtype).element_size()
+    store = torch.empty(rf.rf_cache_store_bytes(len(nk), w.N, D, w.torch_dtype) // el,
+                        dtype=w.torch_dtype, device="cuda")
+    h0 = workloads.make_hidden(w, 0, device="cuda")
+    h1 = workloads.make_hidden(w, 1, device="cuda")
+    k = torch.empty((w.S, w.heads, w.head_dim), dtype=w.torch_dtype, device="cuda")
+    v = torch.empty_like(k)
+    c = rf.rf_cache_init(nk, w.T, w.N, D, w.torch_dtype, 1000.0, store=store, h_full=h0)
+    t = 1000.0
+    n = max(5, args.steps)
+    evs = _events(n)
+    for i in range(n):
+        t -= 3.0
+        evs[i][0].record()
+        rf.rf_cache_shift_store(c, t, store=store, h_full=h1 if i % 2 == 0 else h0)
+        evs[i][1].record()
+    for _ in range(2):
+        rf.rf_cache_project_kv(c, store, k, v, t + 1.0)
+    torch.cuda.synchronize()
+    evp = _events(n)
+    for i in range(n):
+        evp[i][0].record()
+        rf.rf_cache_project_kv(c, store, k, v, t + 1.0)
+        evp[i][1].record()
+    torch.cuda.synchronize()
+    p_ms, s_ms = _avg_ms(evp), _avg_ms(evs)
+    fb = w.N * D * el
+    pb = accounting.cache_projection_bytes(len(nk), fb)
+    sb = accounting.cache_store_bytes(len(nk), fb)
+    p_gbs = pb / (p_ms * 1e-3) / 1e9
+    s_gbs = sb / (s_ms * 1e-3) / 1e9
+    print(f"[bench] rolling cache: projection {p_ms * 1e3:.1f} us ({p_gbs:.0f} GB/s), "
+          f"shift-and-store {s_ms * 1e3:.1f} us ({s_gbs:.0f} GB/s), {len(nk)} frames",
+          file=sys.stderr, flush=True)
+    del store, h0, h1, k, v
+    return {"cached_frames": len(nk), "frame_bytes": fb,
+            "projection": {"bytes": pb, "avg_us": round(p_ms * 1e3, 2), "gbs": round(p_gbs, 1),
+                           "frac_hbm": round(p_gbs / PEAK_HBM_GBS, 4)},
+            "shift_store": {"bytes": sb, "avg_us": round(s_ms * 1e3, 2), "gbs": round(s_gbs, 1),
+                            "frac_hbm": round(s_gbs / PEAK_HBM_GBS, 4)}}
 
 
 def bandwidth(w, q, attn_out, full_out, args):

@@ -8,7 +8,10 @@
  * keyframes and the projected states of the skipped non-keyframes
  * (Sec. 3.2.3-3.2.4; App. B.2). This library provides the calls of that step:
  * keyframe-set normalisation, the latent trajectory projection of Eq. (3),
- * keyframe-query attention, and the frame gather/scatter around it.
+ * keyframe-query attention, and the frame gather/scatter around it; besides
+ * them, the content-aware keyframe selection of Sec. 3.1 (frame similarity and
+ * Alg. 1's scan) and the per-layer rolling cache of App. B.2, whose projected
+ * hidden states are the skipped frames' keys and values.
  *
  * Conventions shared by every call:
  *  - Return value: RF_OK (0) or a negative rf_status. No C++ exception crosses
@@ -19,7 +22,9 @@
  *  - Device buffers are owned by the caller, must stay alive until the stream
  *    has passed the launched work, and are never retained by the library.
  *    Host arrays are read during the call only; the caller may free them when
- *    the call returns. The library allocates no memory.
+ *    the call returns. The library allocates no memory. The one piece of
+ *    state that outlives a call, the rolling cache's bookkeeping, is a struct
+ *    the caller owns and passes in.
  *  - `stream` is a hipStream_t (NULL = the default stream). Calls only enqueue
  *    work; they do not synchronise. Device faults surface at the caller's next
  *    synchronisation, not as a return code.
@@ -239,6 +244,121 @@ int rf_select_keyframes_adaptive(const double *sim, int32_t T, double tau, int32
                                  double dtau, double delta_up, double delta_down, uint32_t flags,
                                  int32_t *keyframe_ids_out, int32_t *num_keyframes_out,
                                  uint8_t *keyframe_mask_out);
+
+/*
+ * Per-layer rolling cache of post-attention hidden states (App. B.2).
+ *
+ * For each cached frame f (the non-keyframes, fixed when the keyframe set is
+ * frozen at the end of warm-up) one layer's cache keeps two hidden states,
+ * h_before and h_after, each the frame's N = rows_per_frame attention-output
+ * rows of D = hidden elements (D = heads * head_dim), with their timesteps
+ * t_before >= t_after. Diffusion timesteps decrease as denoising proceeds.
+ *
+ * The states live in a caller-owned device buffer `store` of 2 * n_cached
+ * frame slots; slot s starts at store + s * frame_bytes (frame_bytes =
+ * N * D * element size), and the i-th cached frame (in increasing frame order)
+ * owns slots 2i and 2i+1. This host struct, also owned by the caller, records
+ * which of the two slots holds which state: moving h_after into h_before at a
+ * denoising step is a change of slot index, not a copy. The struct is plain
+ * data: the calls below read and update it on the host when they are made, so
+ * work enqueued on different streams must be ordered by the caller (the
+ * projection reads the slots its call named; a later shift_store rewrites one
+ * of them).
+ */
+typedef struct rf_rolling_cache {
+    int32_t T;                  /* frames of the video, 1..RF_MAX_FRAMES */
+    int32_t n_cached;           /* cached frames, 1..T */
+    int64_t rows_per_frame;     /* N */
+    int32_t hidden;             /* D */
+    int32_t dtype;              /* RF_BF16 or RF_F32 */
+    int64_t frame_bytes;        /* N * D * element size */
+    uint32_t magic;             /* set by rf_cache_init */
+    int32_t reserved;
+    int16_t before_slot[RF_MAX_FRAMES];  /* slot of h_before of frame f, -1 if f is not cached */
+    int16_t after_slot[RF_MAX_FRAMES];   /* slot of h_after of frame f, -1 if f is not cached */
+    double t_before[RF_MAX_FRAMES];
+    double t_after[RF_MAX_FRAMES];
+} rf_rolling_cache;
+
+/* Bytes of device store a cache of n_cached frames needs (host only):
+   2 * n_cached * rows_per_frame * hidden * element size.
+   Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (n_cached >
+   RF_MAX_FRAMES, size overflow), RF_ERR_UNSUPPORTED (dtype). */
+int rf_cache_store_bytes(int32_t n_cached, int64_t rows_per_frame, int32_t hidden, int32_t dtype,
+                         int64_t *bytes_out);
+
+/*
+ * Initialisation at the end of warm-up (step t_w): h_before = h_after = the
+ * frame's attention output at t_w, t_before = t_after = t_w (App. B.2).
+ *
+ * cache: host struct, overwritten. frames [n]: the frames to cache, strictly
+ * increasing, each in [0, T), 1 <= n <= T. Frame frames[i] gets slots 2i and
+ * 2i+1; both of its indices point at slot 2i.
+ * h_full: device [T*N][D] of dtype (the attention output of all frames at t_w,
+ *   frame-major), or NULL to set up the bookkeeping only, the caller then
+ *   writing slot 2i itself. When h_full is given, the rows of every listed
+ *   frame are copied into its slot 2i of `store` (device, 16-byte aligned, at
+ *   least rf_cache_store_bytes bytes, not overlapping h_full); store is not
+ *   read when h_full is NULL.
+ * hidden * element size must be a multiple of 16. t_w: finite.
+ * Errors: RF_ERR_INVALID_ARG (NULL cache, bad frame list, sizes <= 0,
+ *   non-finite t_w, overlap), RF_ERR_RANGE, RF_ERR_UNSUPPORTED (dtype,
+ *   alignment, row size), RF_ERR_HIP. On error the struct is left unchanged.
+ */
+int rf_cache_init(rf_rolling_cache *cache, void *store, const void *h_full,
+                  const int32_t *frames, int32_t n, int32_t T, int64_t rows_per_frame,
+                  int32_t hidden, int32_t dtype, double t_w, void *stream);
+
+/*
+ * Shift-and-store at a denoising step (a Rhythmic Point) t_denoise (App. B.2):
+ * for each listed frame, h_before <- h_after and t_before <- t_after (slot
+ * indices only), then h_after <- the frame's new attention output, stored in
+ * the frame's other slot, and t_after <- t_denoise.
+ *
+ * frames [n]: cached frames, strictly increasing; frames == NULL (n ignored)
+ *   means every cached frame, the synchronised update of App. B.2.
+ * h_full: device [T*N][D] (this step's attention output of all frames), or
+ *   NULL to update the bookkeeping only (the caller then writes each frame's
+ *   new after slot itself, before the next projection reads it).
+ * t_denoise: finite and strictly below every listed frame's t_after.
+ * Errors: RF_ERR_INVALID_ARG (NULL or uninitialised cache, a frame not cached,
+ *   list not increasing, t_denoise not below t_after, overlap), RF_ERR_RANGE,
+ *   RF_ERR_UNSUPPORTED (alignment), RF_ERR_HIP. On error the struct is left
+ *   unchanged.
+ */
+int rf_cache_shift_store(rf_rolling_cache *cache, void *store, const void *h_full,
+                         const int32_t *frames, int32_t n, double t_denoise, void *stream);
+
+/*
+ * The interpolation weight of frame f at t_skip (host only):
+ *   alpha = (t_before - t_skip) / (t_before - t_after + 1e-8),
+ * in double, kept inside [0, 1]. Right after initialisation (t_before =
+ * t_after) any earlier step clamps to 1; both slots then hold one state.
+ * Errors: RF_ERR_INVALID_ARG (NULL, uninitialised cache, f not cached,
+ *   non-finite t_skip), RF_ERR_RANGE (f outside [0, T)).
+ */
+int rf_cache_alpha(const rf_rolling_cache *cache, int32_t frame, double t_skip, double *alpha_out);
+
+/*
+ * Keys and values of the cached frames at a skipped step t_skip (App. B.2):
+ * for each listed frame f,
+ *   h_hat = (1 - alpha_f) h_before + alpha_f h_after   (alpha_f from rf_cache_alpha),
+ * evaluated per element as fmaf(alpha_f, h_after, (1 - alpha_f) * h_before) in
+ * fp32 with alpha_f rounded once to float (bf16 results rounded to nearest
+ * even), and written to the frame's rows of both k and v: the projected hidden
+ * state serves as the frame's key and its value. Rows of other frames are not
+ * touched; the keyframes' rows keep the keys and values the caller computed.
+ *
+ * store: the cache's device store. k, v: device [T*N][D] of the cache's dtype
+ *   (D = heads * head_dim, the layout rf_keyframe_attention reads), 16-byte
+ *   aligned, overlapping neither each other nor the store.
+ * frames [n]: cached frames, strictly increasing; NULL means every cached frame.
+ * Errors: RF_ERR_INVALID_ARG (NULL, uninitialised cache, a frame not cached,
+ *   list not increasing, non-finite t_skip, overlap), RF_ERR_UNSUPPORTED
+ *   (alignment), RF_ERR_HIP.
+ */
+int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *k, void *v,
+                        const int32_t *frames, int32_t n, double t_skip, void *stream);
 
 #ifdef __cplusplus
 }

@@ -17,7 +17,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "librhymeflow.so")
 ARCH = "gfx950"
 
-SOURCES = ["rf_abi.cpp", "rf_attention.hip", "rf_project.hip", "rf_gather.hip", "rf_similarity.hip"]
+SOURCES = ["rf_abi.cpp", "rf_attention.hip", "rf_project.hip", "rf_gather.hip", "rf_similarity.hip",
+           "rf_cache.hip"]
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

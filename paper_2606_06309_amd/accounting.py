@@ -44,6 +44,19 @@ def gather_bytes(M: int, rows_per_frame: int, row_bytes: int) -> int:
     return 2 * M * rows_per_frame * row_bytes
 
 
+def cache_projection_bytes(n_frames: int, frame_bytes: int) -> int:
+    """Bytes of one rolling-cache projection launch (App. B.2): per projected
+    frame both cached states are read and the result is written as the key
+    and as the value."""
+    return 4 * n_frames * frame_bytes
+
+
+def cache_store_bytes(n_frames: int, frame_bytes: int) -> int:
+    """Bytes of one cache store (initialisation or shift-and-store): each
+    frame's new state read from the attention output and written to its slot."""
+    return 2 * n_frames * frame_bytes
+
+
 # ---------------------------------------------------------------------------
 # the paper's analytic model, App. B.1 (kept as the paper states it)
 # ---------------------------------------------------------------------------

@@ -33,7 +33,27 @@ EXPORTED = [
     "rf_project_latents", "rf_keyframe_attention",
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
+    "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
+    "rf_cache_project_kv",
 ]
+
+
+class rf_rolling_cache(ctypes.Structure):
+    """The C struct rf_rolling_cache (host bookkeeping of one layer's cache)."""
+    _fields_ = [
+        ("T", ctypes.c_int32),
+        ("n_cached", ctypes.c_int32),
+        ("rows_per_frame", ctypes.c_int64),
+        ("hidden", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("frame_bytes", ctypes.c_int64),
+        ("magic", ctypes.c_uint32),
+        ("reserved", ctypes.c_int32),
+        ("before_slot", ctypes.c_int16 * RF_MAX_FRAMES),
+        ("after_slot", ctypes.c_int16 * RF_MAX_FRAMES),
+        ("t_before", ctypes.c_double * RF_MAX_FRAMES),
+        ("t_after", ctypes.c_double * RF_MAX_FRAMES),
+    ]
 
 
 class RhymeFlowError(RuntimeError):
@@ -85,6 +105,18 @@ lib.rf_select_keyframes_adaptive.argtypes = [_dp, _i32, ctypes.c_double, _i32, c
                                              ctypes.c_double, ctypes.c_double, ctypes.c_uint32,
                                              _i32p, _i32p, _u8p]
 lib.rf_select_keyframes_adaptive.restype = ctypes.c_int
+_cachep = ctypes.POINTER(rf_rolling_cache)
+lib.rf_cache_store_bytes.argtypes = [_i32, _i64, _i32, _i32, ctypes.POINTER(_i64)]
+lib.rf_cache_store_bytes.restype = ctypes.c_int
+lib.rf_cache_init.argtypes = [_cachep, _vp, _vp, _i32p, _i32, _i32, _i64, _i32, _i32,
+                              ctypes.c_double, _vp]
+lib.rf_cache_init.restype = ctypes.c_int
+lib.rf_cache_shift_store.argtypes = [_cachep, _vp, _vp, _i32p, _i32, ctypes.c_double, _vp]
+lib.rf_cache_shift_store.restype = ctypes.c_int
+lib.rf_cache_alpha.argtypes = [_cachep, _i32, ctypes.c_double, _dp]
+lib.rf_cache_alpha.restype = ctypes.c_int
+lib.rf_cache_project_kv.argtypes = [_cachep, _vp, _vp, _vp, _i32p, _i32, ctypes.c_double, _vp]
+lib.rf_cache_project_kv.restype = ctypes.c_int
 
 
 def _check(status: int):
@@ -281,3 +313,70 @@ def rf_scatter_frames(src_compact: torch.Tensor, dst_full: torch.Tensor, frame_i
     _check(lib.rf_scatter_frames(_dev(src_compact, "src_compact"), _dev(dst_full, "dst_full"),
                                  ids_p, ids.size, T, rows_per_frame, row_bytes, _stream(stream)))
     return dst_full
+
+
+# --- rolling cache (App. B.2) ------------------------------------------------------
+
+def rf_cache_store_bytes(n_cached: int, rows_per_frame: int, hidden: int, dtype) -> int:
+    """Bytes of device store a cache of n_cached frames needs."""
+    n = _i64(0)
+    code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    _check(lib.rf_cache_store_bytes(n_cached, rows_per_frame, hidden, code, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _frames_arg(frames):
+    if frames is None:
+        return None, None, 0
+    ids, ids_p = _ids(frames)
+    return ids, ids_p, ids.size
+
+
+def _opt_dev(t, name):
+    return None if t is None else _dev(t, name)
+
+
+def rf_cache_init(frames, T: int, rows_per_frame: int, hidden: int, dtype, t_w: float,
+                  store=None, h_full=None, cache=None, stream=None) -> rf_rolling_cache:
+    """Sets up (or overwrites) `cache` for the listed frames at t_w and, when
+    h_full ([T*N][...] device tensor) is given, copies their rows into the store."""
+    cache = rf_rolling_cache() if cache is None else cache
+    ids, ids_p = _ids(frames)
+    code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    _check(lib.rf_cache_init(ctypes.byref(cache), _opt_dev(store, "store"), _opt_dev(h_full, "h_full"),
+                             ids_p if ids.size else None, ids.size, T, rows_per_frame, hidden, code,
+                             float(t_w), _stream(stream) if h_full is not None else None))
+    return cache
+
+
+def rf_cache_shift_store(cache: rf_rolling_cache, t_denoise: float, store=None, h_full=None,
+                         frames=None, stream=None) -> rf_rolling_cache:
+    """Shift-and-store at t_denoise for `frames` (None: every cached frame)."""
+    _, ids_p, n = _frames_arg(frames)
+    _check(lib.rf_cache_shift_store(ctypes.byref(cache), _opt_dev(store, "store"),
+                                    _opt_dev(h_full, "h_full"), ids_p, n, float(t_denoise),
+                                    _stream(stream) if h_full is not None else None))
+    return cache
+
+
+def rf_cache_alpha(cache: rf_rolling_cache, frame: int, t_skip: float) -> float:
+    a = ctypes.c_double(0.0)
+    _check(lib.rf_cache_alpha(ctypes.byref(cache), frame, float(t_skip), ctypes.byref(a)))
+    return a.value
+
+
+def rf_cache_project_kv(cache: rf_rolling_cache, store: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                        t_skip: float, frames=None, stream=None):
+    """Writes the projected hidden state of each listed cached frame (None:
+    all) into its rows of k and v, in place ([T*N][heads][head_dim] tensors)."""
+    for t, name in ((k, "k"), (v, "v")):
+        if t.numel() * t.element_size() != cache.T * cache.frame_bytes:
+            raise ValueError(f"{name} must hold T * rows_per_frame rows of the cache's row size")
+        if _dtype_code(t.dtype) != cache.dtype:
+            raise TypeError(f"{name} must have the cache's dtype")
+    if store.numel() * store.element_size() < 2 * cache.n_cached * cache.frame_bytes:
+        raise ValueError("store is smaller than the cache needs")
+    _, ids_p, n = _frames_arg(frames)
+    _check(lib.rf_cache_project_kv(ctypes.byref(cache), _dev(store, "store"), _dev(k, "k"),
+                                   _dev(v, "v"), ids_p, n, float(t_skip), _stream(stream)))
+    return k, v

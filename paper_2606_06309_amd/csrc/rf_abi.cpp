@@ -238,7 +238,8 @@ static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int3
     if (rows_per_frame <= 0 || row_bytes <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: rows_per_frame and row_bytes must be positive", fn);
     rf::FrameCopyParams p{};
-    const int rc = check_id_list(frame_ids, M, T, p.ids, fn);
+    int32_t ids[RF_MAX_FRAMES];
+    const int rc = check_id_list(frame_ids, M, T, ids, fn);
     if (rc != RF_OK) return rc;
     if (row_bytes % 16 != 0)
         return fail(RF_ERR_UNSUPPORTED, "%s: row_bytes %lld not a multiple of 16", fn,
@@ -253,7 +254,10 @@ static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int3
     p.dst = dst;
     p.frame_bytes = frame_bytes;
     p.M = M;
-    p.scatter = scatter;
+    for (int32_t m = 0; m < M; ++m) {
+        p.src_idx[m] = scatter ? m : ids[m];
+        p.dst_idx[m] = scatter ? ids[m] : m;
+    }
     return launched(rf::launch_frame_copy(p, static_cast<hipStream_t>(stream)), fn);
 }
 
@@ -353,6 +357,223 @@ int rf_select_keyframes_adaptive(const double *sim, int32_t T, double tau, int32
         for (int32_t m = 0; m < n; ++m) keyframe_mask_out[keyframe_ids_out[m]] = 1;
     }
     return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Rolling cache (App. B.2)
+// ---------------------------------------------------------------------------
+
+static const uint32_t kCacheMagic = 0x52464331u;
+static const double kHiddenEps = 1e-8;
+
+static int64_t elem_bytes(int32_t dtype) { return dtype == RF_F32 ? 4 : 2; }
+
+static int cache_store_bytes(int32_t n_cached, int64_t rows_per_frame, int32_t hidden, int32_t dtype,
+                             int64_t *bytes_out, const char *fn) {
+    if (n_cached <= 0 || rows_per_frame <= 0 || hidden <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
+    if (n_cached > RF_MAX_FRAMES)
+        return fail(RF_ERR_RANGE, "%s: n_cached = %d exceeds %d", fn, n_cached, RF_MAX_FRAMES);
+    if (dtype != RF_F32 && dtype != RF_BF16) return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (static_cast<double>(rows_per_frame) * hidden * elem_bytes(dtype) * 2.0 * n_cached * RF_MAX_FRAMES > 4.0e18)
+        return fail(RF_ERR_RANGE, "%s: size overflows", fn);
+    *bytes_out = 2 * static_cast<int64_t>(n_cached) * rows_per_frame * hidden * elem_bytes(dtype);
+    return RF_OK;
+}
+
+int rf_cache_store_bytes(int32_t n_cached, int64_t rows_per_frame, int32_t hidden, int32_t dtype,
+                         int64_t *bytes_out) {
+    const char *fn = "rf_cache_store_bytes";
+    if (!bytes_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    const int rc = cache_store_bytes(n_cached, rows_per_frame, hidden, dtype, bytes_out, fn);
+    return rc == RF_OK ? ok() : rc;
+}
+
+// An initialised cache struct whose sizes and slot indices are consistent.
+static int check_cache(const rf_rolling_cache *c, const char *fn) {
+    if (!c) return fail(RF_ERR_INVALID_ARG, "%s: NULL cache", fn);
+    if (c->magic != kCacheMagic) return fail(RF_ERR_INVALID_ARG, "%s: cache not initialised by rf_cache_init", fn);
+    if (c->T <= 0 || c->T > RF_MAX_FRAMES || c->n_cached <= 0 || c->n_cached > c->T ||
+        c->rows_per_frame <= 0 || c->hidden <= 0 || (c->dtype != RF_F32 && c->dtype != RF_BF16) ||
+        c->frame_bytes != c->rows_per_frame * c->hidden * elem_bytes(c->dtype))
+        return fail(RF_ERR_INVALID_ARG, "%s: cache struct is inconsistent", fn);
+    for (int32_t f = 0; f < c->T; ++f) {
+        const int b = c->before_slot[f], a = c->after_slot[f];
+        if (b < 0 && a < 0) continue;
+        if (b < 0 || a < 0 || b >= 2 * c->n_cached || a >= 2 * c->n_cached || (b >> 1) != (a >> 1))
+            return fail(RF_ERR_INVALID_ARG, "%s: cache struct has bad slots for frame %d", fn, f);
+        if (!isfinite(c->t_before[f]) || !isfinite(c->t_after[f]) || !(c->t_after[f] <= c->t_before[f]))
+            return fail(RF_ERR_INVALID_ARG, "%s: cache struct has bad timesteps for frame %d", fn, f);
+    }
+    return RF_OK;
+}
+
+// The listed frames (NULL: every cached frame), strictly increasing and cached.
+static int cache_frames(const rf_rolling_cache *c, const int32_t *frames, int32_t n, int32_t *out,
+                        int32_t *n_out, const char *fn) {
+    if (!frames) {
+        int32_t k = 0;
+        for (int32_t f = 0; f < c->T; ++f)
+            if (c->after_slot[f] >= 0) out[k++] = f;
+        *n_out = k;
+        return RF_OK;
+    }
+    if (n <= 0 || n > c->T) return fail(RF_ERR_INVALID_ARG, "%s: n = %d outside 1..%d", fn, n, c->T);
+    for (int32_t i = 0; i < n; ++i) {
+        if (frames[i] < 0 || frames[i] >= c->T)
+            return fail(RF_ERR_RANGE, "%s: frame %d outside [0, %d)", fn, frames[i], c->T);
+        if (i > 0 && frames[i] <= frames[i - 1])
+            return fail(RF_ERR_INVALID_ARG, "%s: frames not strictly increasing at position %d", fn, i);
+        if (c->after_slot[frames[i]] < 0) return fail(RF_ERR_INVALID_ARG, "%s: frame %d is not cached", fn, frames[i]);
+        out[i] = frames[i];
+    }
+    *n_out = n;
+    return RF_OK;
+}
+
+// Copies the rows of each listed frame of h_full into its after slot.
+static int store_after(const rf_rolling_cache &c, void *store, const void *h_full, const int32_t *fr,
+                       int32_t n, void *stream, const char *fn) {
+    if (!store) return fail(RF_ERR_INVALID_ARG, "%s: NULL store", fn);
+    if (!aligned16(store) || !aligned16(h_full))
+        return fail(RF_ERR_UNSUPPORTED, "%s: store and h_full must be 16-byte aligned", fn);
+    const int64_t store_bytes = 2 * static_cast<int64_t>(c.n_cached) * c.frame_bytes;
+    if (overlaps(store, store_bytes, h_full, c.frame_bytes * c.T))
+        return fail(RF_ERR_INVALID_ARG, "%s: store overlaps h_full", fn);
+    rf::FrameCopyParams p{};
+    p.src = h_full;
+    p.dst = store;
+    p.frame_bytes = c.frame_bytes;
+    p.M = n;
+    for (int32_t i = 0; i < n; ++i) {
+        p.src_idx[i] = fr[i];
+        p.dst_idx[i] = c.after_slot[fr[i]];
+    }
+    return launched(rf::launch_frame_copy(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_cache_init(rf_rolling_cache *cache, void *store, const void *h_full, const int32_t *frames,
+                  int32_t n, int32_t T, int64_t rows_per_frame, int32_t hidden, int32_t dtype,
+                  double t_w, void *stream) {
+    const char *fn = "rf_cache_init";
+    if (!cache) return fail(RF_ERR_INVALID_ARG, "%s: NULL cache", fn);
+    int32_t ids[RF_MAX_FRAMES];
+    int rc = check_id_list(frames, n, T, ids, fn);
+    if (rc != RF_OK) return rc;
+    int64_t need = 0;
+    rc = cache_store_bytes(n, rows_per_frame, hidden, dtype, &need, fn);
+    if (rc != RF_OK) return rc;
+    if ((static_cast<int64_t>(hidden) * elem_bytes(dtype)) % 16 != 0)
+        return fail(RF_ERR_UNSUPPORTED, "%s: a row of %d elements is not a multiple of 16 bytes", fn, hidden);
+    if (!isfinite(t_w)) return fail(RF_ERR_INVALID_ARG, "%s: t_w must be finite", fn);
+    if (h_full && !store) return fail(RF_ERR_INVALID_ARG, "%s: NULL store", fn);
+
+    rf_rolling_cache c;
+    memset(&c, 0, sizeof c);
+    c.T = T;
+    c.n_cached = n;
+    c.rows_per_frame = rows_per_frame;
+    c.hidden = hidden;
+    c.dtype = dtype;
+    c.frame_bytes = rows_per_frame * hidden * elem_bytes(dtype);
+    c.magic = kCacheMagic;
+    for (int32_t f = 0; f < RF_MAX_FRAMES; ++f) {
+        c.before_slot[f] = c.after_slot[f] = -1;
+        c.t_before[f] = c.t_after[f] = 0.0;
+    }
+    // h_before = h_after = the state at t_w: both indices name slot 2i
+    for (int32_t i = 0; i < n; ++i) {
+        c.before_slot[ids[i]] = c.after_slot[ids[i]] = static_cast<int16_t>(2 * i);
+        c.t_before[ids[i]] = c.t_after[ids[i]] = t_w;
+    }
+    if (h_full) {
+        rc = store_after(c, store, h_full, ids, n, stream, fn);
+        if (rc != RF_OK) return rc;
+    }
+    *cache = c;
+    return ok();
+}
+
+int rf_cache_shift_store(rf_rolling_cache *cache, void *store, const void *h_full, const int32_t *frames,
+                         int32_t n, double t_denoise, void *stream) {
+    const char *fn = "rf_cache_shift_store";
+    int rc = check_cache(cache, fn);
+    if (rc != RF_OK) return rc;
+    int32_t fr[RF_MAX_FRAMES], k = 0;
+    rc = cache_frames(cache, frames, n, fr, &k, fn);
+    if (rc != RF_OK) return rc;
+    if (!isfinite(t_denoise)) return fail(RF_ERR_INVALID_ARG, "%s: t_denoise must be finite", fn);
+    for (int32_t i = 0; i < k; ++i)
+        if (!(t_denoise < cache->t_after[fr[i]]))
+            return fail(RF_ERR_INVALID_ARG, "%s: t_denoise %g is not below t_after %g of frame %d", fn,
+                        t_denoise, cache->t_after[fr[i]], fr[i]);
+    rf_rolling_cache c = *cache;
+    for (int32_t i = 0; i < k; ++i) {
+        const int32_t f = fr[i];
+        // h_before <- h_after, t_before <- t_after; h_after goes to the other slot of the pair
+        c.before_slot[f] = c.after_slot[f];
+        c.t_before[f] = c.t_after[f];
+        c.after_slot[f] = static_cast<int16_t>(c.before_slot[f] ^ 1);
+        c.t_after[f] = t_denoise;
+    }
+    if (h_full) {
+        rc = store_after(c, store, h_full, fr, k, stream, fn);
+        if (rc != RF_OK) return rc;
+    }
+    *cache = c;
+    return ok();
+}
+
+// App. B.2's weight with its epsilon, clamped to [0, 1].
+static double cache_alpha(const rf_rolling_cache &c, int32_t f, double t_skip) {
+    const double a = (c.t_before[f] - t_skip) / (c.t_before[f] - c.t_after[f] + kHiddenEps);
+    return a < 0.0 ? 0.0 : (a > 1.0 ? 1.0 : a);
+}
+
+int rf_cache_alpha(const rf_rolling_cache *cache, int32_t frame, double t_skip, double *alpha_out) {
+    const char *fn = "rf_cache_alpha";
+    int rc = check_cache(cache, fn);
+    if (rc != RF_OK) return rc;
+    if (!alpha_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    if (frame < 0 || frame >= cache->T) return fail(RF_ERR_RANGE, "%s: frame %d outside [0, %d)", fn, frame, cache->T);
+    if (cache->after_slot[frame] < 0) return fail(RF_ERR_INVALID_ARG, "%s: frame %d is not cached", fn, frame);
+    if (!isfinite(t_skip)) return fail(RF_ERR_INVALID_ARG, "%s: t_skip must be finite", fn);
+    *alpha_out = cache_alpha(*cache, frame, t_skip);
+    return ok();
+}
+
+int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *k, void *v,
+                        const int32_t *frames, int32_t n, double t_skip, void *stream) {
+    const char *fn = "rf_cache_project_kv";
+    int rc = check_cache(cache, fn);
+    if (rc != RF_OK) return rc;
+    if (!store || !k || !v) return fail(RF_ERR_INVALID_ARG, "%s: NULL buffer", fn);
+    int32_t fr[RF_MAX_FRAMES], cnt = 0;
+    rc = cache_frames(cache, frames, n, fr, &cnt, fn);
+    if (rc != RF_OK) return rc;
+    if (!isfinite(t_skip)) return fail(RF_ERR_INVALID_ARG, "%s: t_skip must be finite", fn);
+    if (!aligned16(store) || !aligned16(k) || !aligned16(v))
+        return fail(RF_ERR_UNSUPPORTED, "%s: pointers must be 16-byte aligned", fn);
+    const int64_t store_bytes = 2 * static_cast<int64_t>(cache->n_cached) * cache->frame_bytes;
+    const int64_t kv_bytes = cache->frame_bytes * cache->T;
+    if (overlaps(k, kv_bytes, v, kv_bytes) || overlaps(k, kv_bytes, store, store_bytes) ||
+        overlaps(v, kv_bytes, store, store_bytes))
+        return fail(RF_ERR_INVALID_ARG, "%s: k, v and store must not overlap", fn);
+    rf::CacheProjParams p{};
+    p.store = store;
+    p.k = k;
+    p.v = v;
+    p.frame_bytes = cache->frame_bytes;
+    p.n = cnt;
+    p.dtype = cache->dtype;
+    for (int32_t i = 0; i < cnt; ++i) {
+        const int32_t f = fr[i];
+        p.before[i] = cache->before_slot[f];
+        p.after[i] = cache->after_slot[f];
+        p.dst[i] = static_cast<uint8_t>(f);
+        p.alpha[i] = static_cast<float>(cache_alpha(*cache, f, t_skip));
+    }
+    return launched(rf::launch_cache_projection(p, static_cast<hipStream_t>(stream)), fn);
 }
 
 }  // extern "C"

@@ -2,7 +2,8 @@
 //
 // A frame-major token sequence stores each frame as one contiguous block of
 // rows_per_frame rows, so gathering the keyframes' rows is a copy of M
-// contiguous blocks, and scattering is the reverse. Bandwidth-bound: every
+// contiguous blocks, and scattering is the reverse; storing frames into the
+// rolling cache's slots is the same copy with another index pair per block. Bandwidth-bound: every
 // access is a coalesced 16-byte load or store, no LDS, no matrix cores.
 #include "rf_internal.h"
 
@@ -19,16 +20,15 @@ struct CopyKArgs {
     u32x4 *dst;
     int64_t frame_vecs;       // 16-byte vectors per frame
     int32_t blocks_per_frame;
-    int32_t scatter;
-    int32_t ids[kMaxFrames];
+    int32_t src_idx[kMaxFrames];
+    int32_t dst_idx[kMaxFrames];
 };
 
 __global__ __launch_bounds__(kThreads) void frame_copy_kernel(const CopyKArgs a) {
     const int m = blockIdx.x / a.blocks_per_frame;
     const int chunk = blockIdx.x - m * a.blocks_per_frame;
-    const int64_t f = a.ids[m];
-    const int64_t src_frame = a.scatter ? m : f;
-    const int64_t dst_frame = a.scatter ? f : m;
+    const int64_t src_frame = a.src_idx[m];
+    const int64_t dst_frame = a.dst_idx[m];
     const u32x4 *s = a.src + src_frame * a.frame_vecs;
     u32x4 *d = a.dst + dst_frame * a.frame_vecs;
     const int64_t base = static_cast<int64_t>(chunk) * kThreads * kUnroll + threadIdx.x;
@@ -52,8 +52,10 @@ hipError_t launch_frame_copy(const FrameCopyParams &p, hipStream_t stream) {
     a.src = static_cast<const u32x4 *>(p.src);
     a.dst = static_cast<u32x4 *>(p.dst);
     a.frame_vecs = p.frame_bytes / 16;
-    a.scatter = p.scatter;
-    for (int m = 0; m < p.M; ++m) a.ids[m] = p.ids[m];
+    for (int m = 0; m < p.M; ++m) {
+        a.src_idx[m] = p.src_idx[m];
+        a.dst_idx[m] = p.dst_idx[m];
+    }
     const int64_t per_block = static_cast<int64_t>(kThreads) * kUnroll;
     const int64_t bpf = (a.frame_vecs + per_block - 1) / per_block;
     const int64_t blocks = bpf * p.M;

@@ -42,16 +42,37 @@ struct ProjParams {
 
 hipError_t launch_projection(const ProjParams &p, hipStream_t stream);
 
+// Copies of whole frames: block src_idx[m] of src to block dst_idx[m] of dst,
+// m < M, each block frame_bytes long (gather: src_idx = ids, dst_idx = m;
+// scatter: the reverse; rolling-cache store: frame -> cache slot).
 struct FrameCopyParams {
     const void *src;
     void *dst;
     int64_t frame_bytes;      // rows_per_frame * row_bytes
     int32_t M;
-    int32_t scatter;          // 0: full -> compact, 1: compact -> full
-    int32_t ids[kMaxFrames];
+    int32_t src_idx[kMaxFrames];
+    int32_t dst_idx[kMaxFrames];
 };
 
 hipError_t launch_frame_copy(const FrameCopyParams &p, hipStream_t stream);
+
+// Rolling-cache projection (App. B.2): for entry m, frame block dst[m] of both
+// k and v receives fmaf(alpha[m], after, (1 - alpha[m]) * before) of store
+// slots before[m] and after[m].
+struct CacheProjParams {
+    const void *store;
+    void *k;
+    void *v;
+    int64_t frame_bytes;
+    int32_t n;
+    int32_t dtype;
+    int16_t before[kMaxFrames];
+    int16_t after[kMaxFrames];
+    uint8_t dst[kMaxFrames];
+    float alpha[kMaxFrames];
+};
+
+hipError_t launch_cache_projection(const CacheProjParams &p, hipStream_t stream);
 
 // Frame cosine similarity: blocking of the frame Gram matrix over feature
 // chunks (shared by the workspace query and the launcher).

@@ -26,6 +26,9 @@ bf16 (round-to-nearest-even, torch's conversion) for the bf16 workloads.
 Latents: slot 0 then slot 1, fp32 randn from a generator seeded index + 100.
 Latent grids: tiny 4 x 5x16x16; 480p 16 x 21x60x104; the others 16 x T x 2H x 2W.
 Projection timesteps (t_start, t_end, tau) = (24, 21, 23), i.e. alpha = 1/3.
+Cached hidden states (the rolling cache's attention outputs): one
+[S][heads][head_dim] fp32 randn draw per store, generator seeded index + 200 +
+the store's number (0 = the warm-up state), rounded to the workload's dtype.
 """
 from dataclasses import dataclass, field
 from typing import List, Tuple
@@ -158,3 +161,13 @@ def make_scene_latents(B: int, C: int, T: int, H: int, W: int, cut_frames, noise
         base = torch.randn((B, C, 1, H, W), generator=g, device=device)
         x[:, :, start:end] = base + noise * torch.randn((B, C, end - start, H, W), generator=g, device=device)
     return x.to(dtype)
+
+
+def make_hidden(w: Workload, store: int, device="cpu", dtype=None):
+    """Synthetic post-attention hidden states [S][heads][head_dim] for the
+    rolling cache: store 0 is the state cached at the end of warm-up, store
+    k >= 1 the k-th shift-and-store."""
+    g = torch.Generator(device=device)
+    g.manual_seed(w.index + 200 + store)
+    x = torch.randn((w.S, w.heads, w.head_dim), generator=g, device=device, dtype=torch.float32)
+    return x.to(w.torch_dtype if dtype is None else dtype)

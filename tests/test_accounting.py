@@ -87,3 +87,12 @@ def test_byte_counts():
     assert b == 16 * (15 * 3 + 6 * 2) * 6240 * 4
     assert acc.projection_bytes(1, 16, 21, 6240, 6, 4, aliased=True) == 16 * 45 * 6240 * 4
     assert acc.gather_bytes(6, w.N, w.heads * w.head_dim * 2) == 2 * 9360 * 12 * 128 * 2
+
+
+def test_cache_byte_counts():
+    w = workloads.WORKLOADS["long"]
+    # 25 cached frames of 3,600 rows x 3,072 bf16: 22,118,400 bytes each
+    fb = w.N * w.heads * w.head_dim * 2
+    assert fb == 22_118_400
+    assert acc.cache_projection_bytes(25, fb) == 2_211_840_000
+    assert acc.cache_store_bytes(25, fb) == 1_105_920_000
