@@ -13,7 +13,10 @@ for the speedup.
 
 Prints ONE JSON line. `value` is keyframe-query attention TFLOP per second of
 whole-step time; `roofline` describes the attention kernel alone, timed with
-HIP events around each launch on the stream it runs on.
+HIP events around each launch on the stream it runs on. Side sections time the
+bandwidth kernels (projection, gather, scatter), content-aware selection
+(frame similarity and Alg. 1's scan) and the rolling cache of App. B.2
+(projection of cached states into K and V, shift-and-store).
 """
 import argparse
 import json
