@@ -23,7 +23,10 @@ Contents, each written from the paper (RhymeFlow, arXiv 2606.06309):
   post-attention hidden states per non-keyframe with their timesteps,
   initialisation at the end of warm-up, shift-and-store at denoising steps,
   the projection with the epsilon form of alpha at skipped steps, and the
-  key/value sequence in which the projected state is both key and value.
+  key/value sequence in which the projected state is both key and value;
+* the progressive asynchronous schedule (pure Python): Eq. 2's stride and
+  Alg. 2's loop over the denoising steps (warm-up, Rhythmic Points, skipped
+  steps with Eq. 3's interval and weight).
 """
 import ctypes
 import math
@@ -441,3 +444,54 @@ def as_oracle_f64(x) -> np.ndarray:
     if dt == BF16:
         return bf16_bits_to_f64(a).reshape(a.shape)
     return np.array(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# progressive asynchronous schedule (Eq. 2, Alg. 2)
+# ---------------------------------------------------------------------------
+
+def skip_stride(t: int, T: int, T_w: int, T_mid: int, n_small: int, n_large: int) -> int:
+    """Eq. 2: n_small while T_mid < t <= T - T_w, n_large once t <= T_mid.
+    Defined for the asynchronous phase only (t <= T - T_w)."""
+    if t > T - T_w:
+        raise ValueError("warm-up steps have no skip stride")
+    return n_small if t > T_mid else n_large
+
+
+def async_schedule(T: int, T_w: int, T_mid: int, n_small: int, n_large: int):
+    """Alg. 2's loop over t = T down to 1, as a list of per-step dicts.
+
+    Warm-up (t > T - T_w): every frame takes one full step. Afterwards the
+    keyframes take one step at every t; the non-keyframes, all on one shared
+    schedule, take a step of n_skip(t) (Eq. 2; stopping at 0) whenever their
+    state time equals t (a Rhythmic Point, where every frame is updated), and
+    are otherwise skipped, their state at t being projected between the time
+    they last left (t_start) and the time they reached (t_end) with Eq. 3's
+    weight. Each non-keyframe's state time is followed step by step; when the
+    stride never changes between two updates this is Alg. 2's test
+    (T - T_w - t) mod n_skip == 0."""
+    steps = []
+    state = T          # the non-keyframes' state time
+    left = None        # the time of their last update (Eq. 3's t_start)
+    for t in range(T, 0, -1):
+        if t > T - T_w:
+            steps.append(dict(t=t, phase="warmup", n_skip=1, nonkey_to=t - 1,
+                              t_start=None, t_end=None, alpha=None))
+            state = t - 1
+            continue
+        n = skip_stride(t, T, T_w, T_mid, n_small, n_large)
+        if state == t:
+            to = max(t - n, 0)
+            steps.append(dict(t=t, phase="rhythmic", n_skip=n, nonkey_to=to,
+                              t_start=None, t_end=None, alpha=None))
+            left, state = t, to
+        else:
+            steps.append(dict(t=t, phase="skip", n_skip=n, nonkey_to=None, t_start=left,
+                              t_end=state, alpha=(left - t) / (left - state)))
+    return steps
+
+
+def alg2_nonkey_active(t: int, T: int, T_w: int, T_mid: int, n_small: int, n_large: int) -> bool:
+    """Alg. 2's membership test for non-keyframes at an asynchronous step, as
+    printed: (T - T_w - t) mod n_skip(t) == 0."""
+    return (T - T_w - t) % skip_stride(t, T, T_w, T_mid, n_small, n_large) == 0
