@@ -10,8 +10,9 @@
  * keyframe-set normalisation, the latent trajectory projection of Eq. (3),
  * keyframe-query attention, and the frame gather/scatter around it; besides
  * them, the content-aware keyframe selection of Sec. 3.1 (frame similarity and
- * Alg. 1's scan) and the per-layer rolling cache of App. B.2, whose projected
- * hidden states are the skipped frames' keys and values.
+ * Alg. 1's scan), the per-layer rolling cache of App. B.2, whose projected
+ * hidden states are the skipped frames' keys and values, and the progressive
+ * asynchronous schedule (Eq. 2, Alg. 2) that says which step is which.
  *
  * Conventions shared by every call:
  *  - Return value: RF_OK (0) or a negative rf_status. No C++ exception crosses
@@ -359,6 +360,47 @@ int rf_cache_alpha(const rf_rolling_cache *cache, int32_t frame, double t_skip, 
  */
 int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *k, void *v,
                         const int32_t *frames, int32_t n, double t_skip, void *stream);
+
+/*
+ * Progressive asynchronous schedule (Eq. 2; Alg. 2), host only.
+ *
+ * For the denoising steps t = T down to 1: the first T_w steps (t > T - T_w)
+ * are the synchronous warm-up, every frame taking one step with full
+ * attention. Afterwards the keyframes take one step at every t, and the
+ * non-keyframes, which all share one schedule, take a step of
+ * n_skip(t) = n_small if T_mid < t <= T - T_w, n_large if t <= T_mid (Eq. 2),
+ * stopping at 0, whenever their state time equals t. Such a step is a
+ * Rhythmic Point: every frame is updated and attends over every frame. At the
+ * other steps they are skipped: only the keyframes' queries are evaluated and
+ * the non-keyframes' states at t are projected with Eq. (3) on the interval
+ * they are crossing. Following the non-keyframes' state time gives Alg. 2's
+ * test (T - T_w - t) mod n_skip == 0 whenever the stride does not change
+ * between two of their updates, and stays consistent when it does.
+ */
+#define RF_STEP_WARMUP 0     /* every frame one step, full attention */
+#define RF_STEP_RHYTHMIC 1   /* every frame updated, full attention; non-keyframes jump n_skip */
+#define RF_STEP_SKIP 2       /* keyframes only, keyframe-query attention over projected non-keyframes */
+
+typedef struct rf_step_plan {
+    int32_t t;          /* the step: the time keyframes are at before it (T down to 1) */
+    int32_t phase;      /* RF_STEP_WARMUP, RF_STEP_RHYTHMIC or RF_STEP_SKIP */
+    int32_t n_skip;     /* Eq. (2) at t; 1 during warm-up */
+    int32_t nonkey_to;  /* warm-up and Rhythmic Points: the time the non-keyframes reach
+                           (t - 1, resp. max(t - n_skip, 0)); -1 at skipped steps */
+    int32_t t_start;    /* skipped steps: the time the non-keyframes last left (Eq. 3's t_start); else -1 */
+    int32_t t_end;      /* skipped steps: the time they reached (Eq. 3's t_end); else -1 */
+    double alpha;       /* skipped steps: (t_start - t) / (t_start - t_end) in double, in (0, 1); else 0 */
+} rf_step_plan;
+
+/*
+ * T: steps, 1..2^20. T_w, T_mid: 0..T. n_small, n_large: >= 1 (the paper uses
+ * n_small < n_large, e.g. 2 and 3, with T_mid = T/2).
+ * plan_out: host [T] records, step T first. n_rhythmic_out, n_skipped_out
+ * (either may be NULL): counts of Rhythmic Points and of skipped steps.
+ * Errors: RF_ERR_INVALID_ARG (NULL plan, a stride < 1), RF_ERR_RANGE (T, T_w, T_mid).
+ */
+int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, int32_t n_large,
+                      rf_step_plan *plan_out, int32_t *n_rhythmic_out, int32_t *n_skipped_out);
 
 #ifdef __cplusplus
 }

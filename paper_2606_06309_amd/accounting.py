@@ -57,6 +57,25 @@ def cache_store_bytes(n_frames: int, frame_bytes: int) -> int:
     return 2 * n_frames * frame_bytes
 
 
+def schedule_attention_flops(plan, T_frames: int, M: int, N: int, head_dim: int, heads: int):
+    """Attention FLOP of one layer over a whole step plan (Alg. 2): warm-up
+    steps and Rhythmic Points evaluate every frame's queries over all keys,
+    skipped steps only the keyframes' queries (still over all keys).
+    `plan` is a list of per-step dicts with a "phase" of "warmup", "rhythmic"
+    or "skip". Returns the per-phase step counts, FLOP, the dense FLOP (every
+    step full) and their ratio."""
+    S = T_frames * N
+    full = attention_flops(S, S, head_dim, heads)
+    kq = attention_flops(M * N, S, head_dim, heads)
+    counts = {"warmup": 0, "rhythmic": 0, "skip": 0}
+    for step in plan:
+        counts[step["phase"]] += 1
+    total = (counts["warmup"] + counts["rhythmic"]) * full + counts["skip"] * kq
+    dense = len(plan) * full
+    return {"steps": counts, "full_step_flop": full, "skip_step_flop": kq, "flop": total,
+            "dense_flop": dense, "ratio": dense / total if total else float("nan")}
+
+
 # ---------------------------------------------------------------------------
 # the paper's analytic model, App. B.1 (kept as the paper states it)
 # ---------------------------------------------------------------------------

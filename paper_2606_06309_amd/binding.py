@@ -34,8 +34,26 @@ EXPORTED = [
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
-    "rf_cache_project_kv",
+    "rf_cache_project_kv", "rf_async_schedule",
 ]
+
+RF_STEP_WARMUP = 0
+RF_STEP_RHYTHMIC = 1
+RF_STEP_SKIP = 2
+_PHASE_NAMES = {RF_STEP_WARMUP: "warmup", RF_STEP_RHYTHMIC: "rhythmic", RF_STEP_SKIP: "skip"}
+
+
+class rf_step_plan(ctypes.Structure):
+    """The C struct rf_step_plan (one denoising step of the schedule)."""
+    _fields_ = [
+        ("t", ctypes.c_int32),
+        ("phase", ctypes.c_int32),
+        ("n_skip", ctypes.c_int32),
+        ("nonkey_to", ctypes.c_int32),
+        ("t_start", ctypes.c_int32),
+        ("t_end", ctypes.c_int32),
+        ("alpha", ctypes.c_double),
+    ]
 
 
 class rf_rolling_cache(ctypes.Structure):
@@ -117,6 +135,8 @@ lib.rf_cache_alpha.argtypes = [_cachep, _i32, ctypes.c_double, _dp]
 lib.rf_cache_alpha.restype = ctypes.c_int
 lib.rf_cache_project_kv.argtypes = [_cachep, _vp, _vp, _vp, _i32p, _i32, ctypes.c_double, _vp]
 lib.rf_cache_project_kv.restype = ctypes.c_int
+lib.rf_async_schedule.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(rf_step_plan), _i32p, _i32p]
+lib.rf_async_schedule.restype = ctypes.c_int
 
 
 def _check(status: int):
@@ -380,3 +400,21 @@ def rf_cache_project_kv(cache: rf_rolling_cache, store: torch.Tensor, k: torch.T
     _check(lib.rf_cache_project_kv(ctypes.byref(cache), _dev(store, "store"), _dev(k, "k"),
                                    _dev(v, "v"), ids_p, n, float(t_skip), _stream(stream)))
     return k, v
+
+
+# --- asynchronous schedule (Eq. 2, Alg. 2) ----------------------------------------
+
+def rf_async_schedule(T: int, T_w: int, T_mid: int, n_small: int, n_large: int):
+    """The step plan for t = T..1 as a list of dicts (phase as "warmup",
+    "rhythmic" or "skip"; fields that do not apply to a step are None)."""
+    plan = (rf_step_plan * max(T, 1))()
+    nr, ns = _i32(0), _i32(0)
+    _check(lib.rf_async_schedule(T, T_w, T_mid, n_small, n_large, plan, ctypes.byref(nr), ctypes.byref(ns)))
+    out = []
+    for p in plan[:T]:
+        skip = p.phase == RF_STEP_SKIP
+        out.append(dict(t=p.t, phase=_PHASE_NAMES[p.phase], n_skip=p.n_skip,
+                        nonkey_to=None if skip else p.nonkey_to,
+                        t_start=p.t_start if skip else None, t_end=p.t_end if skip else None,
+                        alpha=p.alpha if skip else None))
+    return out

@@ -576,4 +576,52 @@ int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *
     return launched(rf::launch_cache_projection(p, static_cast<hipStream_t>(stream)), fn);
 }
 
+// ---------------------------------------------------------------------------
+// Progressive asynchronous schedule (Eq. 2, Alg. 2)
+// ---------------------------------------------------------------------------
+
+int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, int32_t n_large,
+                      rf_step_plan *plan_out, int32_t *n_rhythmic_out, int32_t *n_skipped_out) {
+    const char *fn = "rf_async_schedule";
+    if (!plan_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL plan", fn);
+    if (T < 1 || T > (1 << 20)) return fail(RF_ERR_RANGE, "%s: T = %d outside 1..%d", fn, T, 1 << 20);
+    if (T_w < 0 || T_w > T) return fail(RF_ERR_RANGE, "%s: T_w = %d outside 0..T", fn, T_w);
+    if (T_mid < 0 || T_mid > T) return fail(RF_ERR_RANGE, "%s: T_mid = %d outside 0..T", fn, T_mid);
+    if (n_small < 1 || n_large < 1)
+        return fail(RF_ERR_INVALID_ARG, "%s: strides must be >= 1 (n_small=%d n_large=%d)", fn, n_small, n_large);
+    int32_t state = T;   // the non-keyframes' state time
+    int32_t left = -1;   // the time of their last update
+    int32_t n_rp = 0, n_sk = 0;
+    for (int32_t t = T, i = 0; t >= 1; --t, ++i) {
+        rf_step_plan p;
+        p.t = t;
+        p.nonkey_to = p.t_start = p.t_end = -1;
+        p.alpha = 0.0;
+        if (t > T - T_w) {  // synchronous warm-up
+            p.phase = RF_STEP_WARMUP;
+            p.n_skip = 1;
+            p.nonkey_to = state = t - 1;
+        } else {
+            p.n_skip = t > T_mid ? n_small : n_large;   // Eq. (2)
+            if (state == t) {  // the non-keyframes are at t: a Rhythmic Point
+                p.phase = RF_STEP_RHYTHMIC;
+                p.nonkey_to = t - p.n_skip > 0 ? t - p.n_skip : 0;
+                left = t;
+                state = p.nonkey_to;
+                ++n_rp;
+            } else {           // skipped: project on the interval [state, left]
+                p.phase = RF_STEP_SKIP;
+                p.t_start = left;
+                p.t_end = state;
+                p.alpha = static_cast<double>(left - t) / static_cast<double>(left - state);
+                ++n_sk;
+            }
+        }
+        plan_out[i] = p;
+    }
+    if (n_rhythmic_out) *n_rhythmic_out = n_rp;
+    if (n_skipped_out) *n_skipped_out = n_sk;
+    return ok();
+}
+
 }  // extern "C"

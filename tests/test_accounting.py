@@ -14,6 +14,8 @@ import pytest
 from paper_2606_06309_amd import accounting as acc
 from paper_2606_06309_amd import workloads
 
+import oracle
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "flops_wan21.json")
 
 
@@ -96,3 +98,18 @@ def test_cache_byte_counts():
     assert fb == 22_118_400
     assert acc.cache_projection_bytes(25, fb) == 2_211_840_000
     assert acc.cache_store_bytes(25, fb) == 1_105_920_000
+
+
+def test_schedule_ledger():
+    # T = 50 steps, T_w = 8, strides 2 / 3 at T_mid = 25: 8 warm-up, 17 Rhythmic Points, 25 skipped
+    plan = oracle.async_schedule(50, 8, 25, 2, 3)
+    w = workloads.WORKLOADS["long"]
+    led = acc.schedule_attention_flops(plan, w.T, w.M, w.N, w.head_dim, w.heads)
+    assert led["steps"] == {"warmup": 8, "rhythmic": 17, "skip": 25}
+    S = w.S
+    full = 4 * S * S * 128 * 24
+    kq = 4 * 8 * 3600 * S * 128 * 24
+    assert led["full_step_flop"] == full and led["skip_step_flop"] == kq
+    assert led["flop"] == 25 * full + 25 * kq and led["dense_flop"] == 50 * full
+    # 50 / (25 + 25 * 8/33) = 1.6097...
+    assert abs(led["ratio"] - 50.0 / (25.0 + 25.0 * 8.0 / 33.0)) < 1e-12
