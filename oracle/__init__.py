@@ -26,7 +26,9 @@ Contents, each written from the paper (RhymeFlow, arXiv 2606.06309):
   key/value sequence in which the projected state is both key and value;
 * the progressive asynchronous schedule (pure Python): Eq. 2's stride and
   Alg. 2's loop over the denoising steps (warm-up, Rhythmic Points, skipped
-  steps with Eq. 3's interval and weight).
+  steps with Eq. 3's interval and weight);
+* attention under a frame-level key/value mask (the keys of listed frames
+  only), through the same C attention routine on the selected keys.
 """
 import ctypes
 import math
@@ -495,3 +497,32 @@ def alg2_nonkey_active(t: int, T: int, T_w: int, T_mid: int, n_small: int, n_lar
     """Alg. 2's membership test for non-keyframes at an asynchronous step, as
     printed: (T - T_w - t) mod n_skip(t) == 0."""
     return (T - T_w - t) % skip_stride(t, T, T_w, T_mid, n_small, n_large) == 0
+
+
+# ---------------------------------------------------------------------------
+# frame-level key/value mask (the frame mask M_Rhyme; Sec. 4's ablations)
+# ---------------------------------------------------------------------------
+
+def frame_attention(q, k, v, q_frames, kv_frames, N: int, rows=None, heads=None):
+    """Attention under a frame-level mask: the query rows are the tokens of
+    q_frames (compact order, as keyframe_attention), the keys and values are
+    the tokens of kv_frames only; every other key is masked out. This is the
+    frame mask M_Rhyme with one key set for all query frames (the Discussions
+    on combining it with a token mask), and with kv_frames = the keyframes it
+    is the keyframe-only ("w/o projection") attention of Sec. 4's ablations.
+    Written as the definition: the masked keys are removed before the fp64
+    softmax. Returns [len(rows)][len(heads)][d] float64."""
+    ka, dk = as_oracle_array(k)
+    va, dv = as_oracle_array(v)
+    kv_tok = rowmap(kv_frames, N)
+    kc = np.ascontiguousarray(ka[kv_tok])
+    vc = np.ascontiguousarray(va[kv_tok])
+    qa, _ = as_oracle_array(q)
+    n_heads = qa.shape[1]
+    rm = rowmap(q_frames, N)
+    rows = np.arange(rm.size) if rows is None else np.asarray(rows, np.int64)
+    heads = np.arange(n_heads) if heads is None else np.asarray(heads, np.int64)
+    tok = np.repeat(rm[rows], heads.size)
+    hd = np.tile(heads, rows.size)
+    res = attention_pairs(qa, kc, vc, tok, hd)
+    return res.reshape(rows.size, heads.size, res.shape[1])
