@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-bandwidth", action="store_true")
     ap.add_argument("--no-selection", action="store_true")
     ap.add_argument("--no-cache", action="store_true")
+    ap.add_argument("--no-schedule", action="store_true")
+    ap.add_argument("--schedule", default="50,8,25,2,3",
+                    help="T,T_w,T_mid,n_small,n_large of the multi-step schedule loop")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU work of the oracle baseline sample")
     return ap.parse_args()
@@ -222,6 +225,9 @@ def main():
     if not args.no_cache:
         result["rolling_cache"] = rolling_cache(w, args)
 
+    if not args.no_schedule:
+        result["schedule"] = schedule_loop(w, args)
+
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
@@ -265,6 +271,57 @@ def selection(w, args):
     return {"similarity_avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "scan_us": round(scan_us, 1),
             "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
+
+
+def schedule_loop(w, args):
+    """A whole denoising schedule (Eq. 2, Alg. 2) at the workload's shape,
+    attention path only: warm-up steps and Rhythmic Points run attention with
+    every frame's queries; skipped steps project the non-keyframe latents
+    (Eq. 3, with the plan's interval and time) and run keyframe-query
+    attention plus the scatter. Q/K/V alternate between two seeded sets. The
+    same number of all-frame attention launches is timed as the dense
+    reference; `ideal` is the FLOP ratio of the plan."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    T_steps, T_w, T_mid, n_s, n_l = (int(x) for x in args.schedule.split(","))
+    plan = rf.rf_async_schedule(T_steps, T_w, T_mid, n_s, n_l)
+    ids, mask = rf.rf_select_keyframes(w.keyframes, w.T)
+    all_ids = list(range(w.T))
+    sets = [workloads.make_qkv(w, device="cuda", seed=900 + i) for i in range(2)]
+    lat = workloads.make_latents(w, B=1, device="cuda")
+    Hl, Wl = w.latent_hw
+    proj = torch.empty((1, w.latent_c, w.T, Hl, Wl), dtype=lat.dtype, device="cuda")
+    kq_out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=sets[0][0].dtype, device="cuda")
+    full_out = torch.empty((w.S, w.heads, w.head_dim), dtype=sets[0][0].dtype, device="cuda")
+
+    def run(dense):
+        for i, step in enumerate(plan):
+            q, k, v = sets[i % 2]
+            if dense or step["phase"] != "skip":
+                rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=full_out)
+            else:
+                rf.rf_project_latents(lat, (step["t_start"], step["t_end"], step["t"]), mask, out=proj)
+                rf.rf_keyframe_attention(q, k, v, ids, w.T, w.H, w.W, out=kq_out)
+                rf.rf_scatter_frames(kq_out, full_out, ids, w.T, w.N)
+
+    times = {}
+    for dense in (False, True):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        run(dense)
+        b.record()
+        torch.cuda.synchronize()
+        times[dense] = a.elapsed_time(b)
+        print(f"[bench] schedule loop ({'dense' if dense else 'asynchronous'}): {times[dense]:.1f} ms",
+              file=sys.stderr, flush=True)
+    led = accounting.schedule_attention_flops(plan, w.T, w.M, w.N, w.head_dim, w.heads)
+    del sets, lat, proj, kq_out, full_out
+    return {"T_steps": T_steps, "T_w": T_w, "T_mid": T_mid, "n_small": n_s, "n_large": n_l,
+            "steps": led["steps"], "async_ms": round(times[False], 2), "dense_ms": round(times[True], 2),
+            "speedup": round(times[True] / times[False], 4), "ideal_flop_ratio": round(led["ratio"], 4),
+            "tflops_async": round(led["flop"] / (times[False] * 1e-3) / 1e12, 1)}
 
 
 def rolling_cache(w, args):

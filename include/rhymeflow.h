@@ -162,6 +162,29 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
                           int32_t dtype, void *stream);
 
 /*
+ * Attention under a frame-level key/value mask: the frame mask M_Rhyme (in
+ * the Discussions, a per-step frame mask that can be multiplied with a token
+ * mask) with one key set for all query frames. The query rows are the tokens
+ * of frames q_frames, as in rf_keyframe_attention; the keys and values are the
+ * tokens of frames kv_frames only, every other key being masked out:
+ *   out = softmax(Q_q K_kv^T / sqrt(head_dim)) V_kv.
+ * kv_frames = the keyframes gives the keyframe-only attention of Sec. 4's
+ * ablations ("w/ keyframe-only attention"; "w/o projection", where keyframes
+ * attend to the synchronised frames only). Masked frames' keys and values are
+ * never read. The kernel walks the listed frames in key tiles that do not
+ * cross a frame, so when N is not a multiple of 64 each frame's last tile is
+ * partly idle.
+ *
+ * kv_frames [Mkv]: strictly increasing, each in [0, T), 1 <= Mkv <= T (Mkv = T
+ * is rf_keyframe_attention). All other arguments, layouts and errors as
+ * rf_keyframe_attention (q_frames / Mq are its keyframe_ids / M).
+ */
+int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
+                       const int32_t *q_frames, int32_t Mq, const int32_t *kv_frames, int32_t Mkv,
+                       int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                       int32_t dtype, void *stream);
+
+/*
  * Frame gather: dst_compact[m*N + n] = src_full[frame_ids[m]*N + n] for rows
  * of row_bytes bytes, N = rows_per_frame; every frame is one contiguous block
  * of N rows (the token layout of a frame-major sequence, App. B.1: S = F x N).

@@ -30,7 +30,7 @@ RF_MAX_FRAMES = 256
 EXPORTED = [
     "rf_status_string", "rf_last_error", "rf_abi_version",
     "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
-    "rf_project_latents", "rf_keyframe_attention",
+    "rf_project_latents", "rf_keyframe_attention", "rf_frame_attention",
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
@@ -111,6 +111,9 @@ lib.rf_project_latents.restype = ctypes.c_int
 lib.rf_keyframe_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
                                       _i32, _i32, _i32, _vp]
 lib.rf_keyframe_attention.restype = ctypes.c_int
+lib.rf_frame_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32p, _i32, _i32, _i32, _i32,
+                                   _i32, _i32, _i32, _vp]
+lib.rf_frame_attention.restype = ctypes.c_int
 lib.rf_gather_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
 lib.rf_gather_frames.restype = ctypes.c_int
 lib.rf_scatter_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
@@ -276,6 +279,29 @@ def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=Non
     _check(lib.rf_keyframe_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                      ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
                                      _stream(stream)))
+    return out
+
+
+def rf_frame_attention(q, k, v, q_frames, kv_frames, T: int, H: int, W: int, out=None, stream=None):
+    """Attention of the tokens of q_frames over the keys/values of kv_frames
+    only; q, k, v [T*H*W][heads][head_dim] -> out [Mq*H*W][heads][head_dim]."""
+    if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share a dtype")
+    S, heads, d = q.shape
+    if S != T * H * W:
+        raise ValueError(f"S = {S} differs from T*H*W = {T * H * W}")
+    ids, ids_p = _ids(q_frames)
+    kv, kv_p = _ids(kv_frames)
+    M = ids.size
+    if out is None:
+        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+    if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
+        raise ValueError("out must be [Mq*H*W][heads][head_dim] of q's dtype")
+    _check(lib.rf_frame_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                  ids_p, M, kv_p, kv.size, T, H, W, heads, d, _dtype_code(q.dtype),
+                                  _stream(stream)))
     return out
 
 

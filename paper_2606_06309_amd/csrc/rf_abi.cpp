@@ -190,18 +190,22 @@ int rf_project_latents(const void *latents, void *out, const double timesteps[3]
     return launched(rf::launch_projection(p, static_cast<hipStream_t>(stream)), fn);
 }
 
-int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out,
-                          const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H,
-                          int32_t W, int32_t heads, int32_t head_dim, int32_t dtype,
-                          void *stream) {
-    const char *fn = "rf_keyframe_attention";
+// Shared validation and launch of the two attention entry points.
+static int attention_call(const void *q, const void *k, const void *v, void *out, const int32_t *q_ids,
+                          int32_t M, const int32_t *kv_ids, int32_t Mkv, int32_t T, int32_t H, int32_t W,
+                          int32_t heads, int32_t head_dim, int32_t dtype, void *stream, const char *fn) {
     if (!q || !k || !v || !out) return fail(RF_ERR_INVALID_ARG, "%s: NULL tensor", fn);
     if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
                     fn, H, W, heads, head_dim);
     rf::AttnParams p{};
-    const int rc = check_id_list(keyframe_ids, M, T, p.kf, fn);
+    int rc = check_id_list(q_ids, M, T, p.kf, fn);
     if (rc != RF_OK) return rc;
+    int32_t kvf[RF_MAX_FRAMES];
+    if (kv_ids) {
+        rc = check_id_list(kv_ids, Mkv, T, kvf, fn);
+        if (rc != RF_OK) return rc;
+    }
     if (head_dim != 64 && head_dim != 128)
         return fail(RF_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
     if (dtype != RF_BF16 && dtype != RF_F32)
@@ -228,7 +232,28 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
     p.heads = heads;
     p.head_dim = head_dim;
     p.dtype = dtype;
+    // every frame listed: the unmasked kernel
+    p.n_kv = (kv_ids && Mkv < T) ? Mkv : 0;
+    for (int32_t i = 0; i < p.n_kv; ++i) p.kvf[i] = kvf[i];
     return launched(rf::launch_attention(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out,
+                          const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H,
+                          int32_t W, int32_t heads, int32_t head_dim, int32_t dtype,
+                          void *stream) {
+    return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype,
+                          stream, "rf_keyframe_attention");
+}
+
+int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
+                       const int32_t *q_frames, int32_t Mq, const int32_t *kv_frames, int32_t Mkv,
+                       int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                       int32_t dtype, void *stream) {
+    const char *fn = "rf_frame_attention";
+    if (!kv_frames) return fail(RF_ERR_INVALID_ARG, "%s: kv_frames is NULL", fn);
+    return attention_call(q, k, v, out, q_frames, Mq, kv_frames, Mkv, T, H, W, heads, head_dim, dtype,
+                          stream, fn);
 }
 
 static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int32_t M, int32_t T,

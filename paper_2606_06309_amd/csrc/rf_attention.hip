@@ -93,6 +93,12 @@ struct AttnKArgs {
     int32_t per_xcd;
     float scale_log2;   // log2(e) / sqrt(d)
     int32_t kf[kMaxFrames];
+    // key/value frame list (frame-masked form only): the keys are the tokens
+    // of frames kvf[0..n_kv), walked frame by frame in tiles that never cross
+    // a frame (tiles_per_frame = ceil(N / kBc); a frame's last tile is partial)
+    int32_t n_kv;
+    int32_t tiles_per_frame;
+    int32_t kvf[kMaxFrames];
 };
 
 // Word 3 of a raw (untyped, stride 0) buffer resource on gfx9-class GPUs.
@@ -253,9 +259,13 @@ __device__ __forceinline__ void pv_tile(const uint8_t *vb, const int (&vofs)[D /
 //   math on tile t
 //   wait for this wave's loads, barrier (tile t+1 visible, tile t released)
 // The loads go through raw buffer resources rebased per tile in scalar
-// registers; the hardware range check zero-fills keys >= S. The loop is
+// registers whose range ends at the tile's last valid key, so the hardware
+// range check zero-fills the keys past it (keys >= S, or past the end of a
+// frame in the frame-masked form) and their scores are masked. The loop is
 // unrolled by two so every LDS access names its buffer statically.
-template <int D>
+// kKvList: the keys are the tokens of the frames a.kvf (a frame-level mask);
+// otherwise all S tokens in order.
+template <int D, bool kKvList>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnKArgs a) {
     using L = TileLayout<D>;
@@ -329,16 +339,37 @@ void attn_bf16_kernel(const AttnKArgs a) {
     // bytes from a head's first element to one past the last element it owns
     const int64_t head_bytes = ((a.S - 1) * rs + D) * 2;
 
-    auto issue = [&](int64_t j0, uint8_t *kdst, uint8_t *vdst) {
-        // The resources start at key j0; their range ends at the head's last key (clamped to
-        // 2^31 - 1: a tile never reaches that far past its first key).
-        const int64_t left = head_bytes - j0 * rs * 2;
+    // Tile t: its first key's token, the bytes from there to the end of its last
+    // valid key, and the number of valid keys (at most kBc).
+    struct Geom {
+        int64_t tok0, left;
+        int32_t valid;
+    };
+    auto geom = [&](int64_t t) {
+        Geom g;
+        if constexpr (kKvList) {
+            const int32_t m = static_cast<int32_t>(t) / a.tiles_per_frame;
+            const int64_t o = (t - static_cast<int64_t>(m) * a.tiles_per_frame) * kBc;
+            g.tok0 = static_cast<int64_t>(a.kvf[m]) * a.N + o;
+            g.valid = static_cast<int32_t>(a.N - o < kBc ? a.N - o : kBc);
+            g.left = ((g.valid - 1) * rs + D) * 2;
+        } else {
+            g.tok0 = t * kBc;
+            g.left = head_bytes - g.tok0 * rs * 2;
+            g.valid = static_cast<int32_t>(a.S - g.tok0 < kBc ? a.S - g.tok0 : kBc);
+        }
+        return g;
+    };
+
+    auto issue = [&](const Geom &g, uint8_t *kdst, uint8_t *vdst) {
+        // The resources start at the tile's first key; their range ends at its last valid
+        // key (clamped to 2^31 - 1: a tile never reaches that far past its first key).
         const int32_t rec = __builtin_amdgcn_readfirstlane(
-            static_cast<int32_t>(left < 0x7fffffffLL ? left : 0x7fffffffLL));
+            static_cast<int32_t>(g.left < 0x7fffffffLL ? g.left : 0x7fffffffLL));
         const __amdgpu_buffer_rsrc_t kr =
-            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + j0 * rs), 0, rec, kBufferWord3);
+            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + g.tok0 * rs), 0, rec, kBufferWord3);
         const __amdgpu_buffer_rsrc_t vr =
-            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(vbase + j0 * rs), 0, rec, kBufferWord3);
+            __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(vbase + g.tok0 * rs), 0, rec, kBufferWord3);
 #pragma unroll
         for (int i = 0; i < kLoadsPerWave; ++i) {
             const int chunk = (wave * kLoadsPerWave + i) * 1024;
@@ -348,18 +379,18 @@ void attn_bf16_kernel(const AttnKArgs a) {
     };
 
     const float sl2 = a.scale_log2;
-    auto compute = [&](int64_t j0, const uint8_t *kb, const uint8_t *vb) {
+    auto compute = [&](int32_t valid, const uint8_t *kb, const uint8_t *vb) {
         // ---- S^T = K Q^T : 32-key blocks ----
         f32x16_t sacc[kNB];
         scores_tile<D, kNB>(kb, kofs, qf, sacc);
         // accumulator r of block b holds key b*32 + (r/4)*8 + grp*4 + r%4 for query `col`
-        if (j0 + kBc > a.S) {
+        if (valid < kBc) {
 #pragma unroll
             for (int b = 0; b < kNB; ++b)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int64_t key = j0 + b * 32 + (r / 4) * 8 + grp * 4 + (r % 4);
-                    if (key >= a.S) sacc[b][r] = -__builtin_huge_valf();
+                    const int key = b * 32 + (r / 4) * 8 + grp * 4 + (r % 4);
+                    if (key >= valid) sacc[b][r] = -__builtin_huge_valf();
                 }
         }
 
@@ -419,16 +450,24 @@ void attn_bf16_kernel(const AttnKArgs a) {
         __syncthreads();
     };
 
-    const int64_t ntiles = (a.S + kBc - 1) / kBc;
-    issue(0, k0, v0);
+    const int64_t ntiles = kKvList ? static_cast<int64_t>(a.n_kv) * a.tiles_per_frame : (a.S + kBc - 1) / kBc;
+    Geom cur = geom(0);
+    issue(cur, k0, v0);
     tile_done();
     for (int64_t t = 0; t < ntiles; t += 2) {
-        if (t + 1 < ntiles) issue((t + 1) * kBc, k1, v1);
-        compute(t * kBc, k0, v0);
+        Geom nxt = cur;
+        if (t + 1 < ntiles) {
+            nxt = geom(t + 1);
+            issue(nxt, k1, v1);
+        }
+        compute(cur.valid, k0, v0);
         tile_done();
         if (t + 1 >= ntiles) break;
-        if (t + 2 < ntiles) issue((t + 2) * kBc, k0, v0);
-        compute((t + 1) * kBc, k1, v1);
+        if (t + 2 < ntiles) {
+            cur = geom(t + 2);
+            issue(cur, k0, v0);
+        }
+        compute(nxt.valid, k1, v1);
         tile_done();
     }
 
@@ -470,6 +509,8 @@ struct AttnF32Args {
     int32_t heads;
     float scale;       // 1 / sqrt(d)
     int32_t kf[kMaxFrames];
+    int32_t n_kv;      // > 0: the keys are the tokens of frames kvf[0..n_kv), S = n_kv * N
+    int32_t kvf[kMaxFrames];
 };
 
 template <int D>
@@ -503,7 +544,12 @@ __global__ __launch_bounds__(2 * kF32Rows) void attn_f32_kernel(const AttnF32Arg
         for (int i = tid; i < kF32Keys * D; i += 2 * kF32Rows) {
             const int key = i / D, c = i % D;
             const int64_t j = j0 + key;
-            const int64_t off = j * rs + static_cast<int64_t>(head) * D + c;
+            int64_t tok = j;
+            if (a.n_kv > 0 && j < a.S) {
+                const int64_t m = j / a.N;
+                tok = static_cast<int64_t>(a.kvf[m]) * a.N + (j - m * a.N);
+            }
+            const int64_t off = tok * rs + static_cast<int64_t>(head) * D + c;
             ks[key][c] = j < a.S ? a.k[off] : 0.0f;
             vs[key][c] = j < a.S ? a.v[off] : 0.0f;
         }
@@ -566,9 +612,19 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         a.per_xcd = static_cast<int32_t>(per_xcd);
         a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(p.head_dim)));
         for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
+        a.n_kv = p.n_kv;
+        a.tiles_per_frame = static_cast<int32_t>((p.N + kBc - 1) / kBc);
+        for (int i = 0; i < p.n_kv; ++i) a.kvf[i] = p.kvf[i];
+        if (p.n_kv > 0 && static_cast<int64_t>(p.n_kv) * a.tiles_per_frame > 0x7fffffffLL)
+            return hipErrorInvalidConfiguration;
         const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds)), block(kThreads);
-        if (p.head_dim == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, stream, a);
-        else hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, stream, a);
+        if (p.n_kv > 0) {
+            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);
+        } else {
+            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, stream, a);
+        }
         return hipGetLastError();
     }
     AttnF32Args a{};
@@ -582,6 +638,9 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
     a.heads = p.heads;
     a.scale = static_cast<float>(1.0 / sqrt(static_cast<double>(p.head_dim)));
     for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
+    a.n_kv = p.n_kv;
+    for (int i = 0; i < p.n_kv; ++i) a.kvf[i] = p.kvf[i];
+    if (p.n_kv > 0) a.S = static_cast<int64_t>(p.n_kv) * p.N;
     const int64_t nq = (Mq + kF32Rows - 1) / kF32Rows;
     if (nq > 0x7fffffffLL || p.heads > 65535) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<uint32_t>(nq), static_cast<uint32_t>(p.heads)), block(2 * kF32Rows);

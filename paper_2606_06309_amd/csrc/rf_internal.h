@@ -25,6 +25,9 @@ struct AttnParams {
     int32_t head_dim;
     int32_t dtype;    // RF_BF16 or RF_F32
     int32_t kf[kMaxFrames];
+    // 0: keys are all S tokens; > 0: only the tokens of frames kvf[0..n_kv)
+    int32_t n_kv;
+    int32_t kvf[kMaxFrames];
 };
 
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream);

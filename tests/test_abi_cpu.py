@@ -141,6 +141,31 @@ def test_attention_validation(kwargs, status):
     assert lib.rf_last_error().decode().startswith("rf_keyframe_attention")
 
 
+def _fattn(q=A, k=B_, v=C_, out=O_, ids=(0, 2, 4), kv=(0, 2, 4), T=5, H=8, W=8, heads=2, d=64,
+           dtype=rf.RF_BF16):
+    arr = (ctypes.c_int32 * max(1, len(ids)))(*ids)
+    kva = (ctypes.c_int32 * max(1, len(kv)))(*kv) if kv is not None else None
+    return lib.rf_frame_attention(q, k, v, out, arr, len(ids), kva, 0 if kv is None else len(kv), T, H, W,
+                                  heads, d, dtype, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(kv=None), rf.RF_ERR_INVALID_ARG),
+    (dict(kv=()), rf.RF_ERR_INVALID_ARG),
+    (dict(kv=(2, 2)), rf.RF_ERR_INVALID_ARG),
+    (dict(kv=(3, 1)), rf.RF_ERR_INVALID_ARG),
+    (dict(kv=(0, 5)), rf.RF_ERR_RANGE),
+    (dict(kv=(0, 1, 2, 3, 4, 5)), rf.RF_ERR_RANGE),
+    (dict(ids=(4, 1)), rf.RF_ERR_INVALID_ARG),
+    (dict(d=96), rf.RF_ERR_UNSUPPORTED),
+    (dict(k=B_ + 8), rf.RF_ERR_UNSUPPORTED),
+    (dict(out=A + 64), rf.RF_ERR_INVALID_ARG),
+])
+def test_frame_attention_validation(kwargs, status):
+    assert _fattn(**kwargs) == status
+    assert lib.rf_last_error().decode().startswith("rf_frame_attention")
+
+
 def _proj(lat=A, out=B_, ts=(24.0, 21.0, 23.0), mask=(1, 0, 1, 0, 1), B=1, C=4, T=5, Hl=16,
           Wl=16, dtype=rf.RF_F32):
     t = (ctypes.c_double * 3)(*ts)
