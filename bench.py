@@ -15,8 +15,10 @@ Prints ONE JSON line. `value` is keyframe-query attention TFLOP per second of
 whole-step time; `roofline` describes the attention kernel alone, timed with
 HIP events around each launch on the stream it runs on. Side sections time the
 bandwidth kernels (projection, gather, scatter), content-aware selection
-(frame similarity and Alg. 1's scan) and the rolling cache of App. B.2
-(projection of cached states into K and V, shift-and-store).
+(frame similarity and Alg. 1's scan), the rolling cache of App. B.2
+(projection of cached states into K and V, shift-and-store), keyframe-only
+attention (a frame-level key/value mask) and a whole denoising schedule of
+Alg. 2 (attention path only) against its dense counterpart.
 """
 import argparse
 import json
@@ -46,6 +48,7 @@ def parse():
     ap.add_argument("--no-selection", action="store_true")
     ap.add_argument("--no-cache", action="store_true")
     ap.add_argument("--no-schedule", action="store_true")
+    ap.add_argument("--no-frame-mask", action="store_true")
     ap.add_argument("--schedule", default="50,8,25,2,3",
                     help="T,T_w,T_mid,n_small,n_large of the multi-step schedule loop")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -225,6 +228,9 @@ def main():
     if not args.no_cache:
         result["rolling_cache"] = rolling_cache(w, args)
 
+    if not args.no_frame_mask:
+        result["frame_mask"] = frame_mask(w, q, k, v, args)
+
     if not args.no_schedule:
         result["schedule"] = schedule_loop(w, args)
 
@@ -271,6 +277,32 @@ def selection(w, args):
     return {"similarity_avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "scan_us": round(scan_us, 1),
             "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
+
+
+def frame_mask(w, q, k, v, args):
+    """Keyframe-only attention (a frame-level key/value mask; Sec. 4's
+    ablations): the keyframes' queries over the keyframes' keys only, timed
+    like the main attention launch."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf
+
+    out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=q.dtype, device="cuda")
+    rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out)
+    torch.cuda.synchronize()
+    n = max(3, args.steps)
+    ev = _events(n)
+    for a, b in ev:
+        a.record()
+        rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out)
+        b.record()
+    torch.cuda.synchronize()
+    ms = _avg_ms(ev)
+    flop = accounting.attention_flops(w.M * w.N, w.M * w.N, w.head_dim, w.heads)
+    tf = flop / (ms * 1e-3) / 1e12
+    print(f"[bench] keyframe-only attention: {ms:.3f} ms = {tf:.1f} TFLOP/s", file=sys.stderr, flush=True)
+    del out
+    return {"kv_frames": list(w.keyframes), "avg_ms": round(ms, 4), "tflops": round(tf, 2),
+            "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop}
 
 
 def schedule_loop(w, args):
