@@ -146,6 +146,10 @@ def main():
     Mq = w.M * w.N
     attn_out = torch.empty((Mq, w.heads, w.head_dim), dtype=q.dtype, device=dev)
     full_out = torch.zeros((w.S, w.heads, w.head_dim), dtype=q.dtype, device=dev)
+    # split-key tail workspace, sized for the largest launch (the all-frame comparator or this step)
+    ws = torch.empty(max(16, rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype),
+                         rf.rf_attention_workspace(w.T, w.T, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype)),
+                     dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
     def step(ev=None):
@@ -153,7 +157,7 @@ def main():
         rf.rf_project_latents(lat, w.timesteps, mask, out=proj_out)
         if ev is not None:
             ev[0].record()
-        rf.rf_keyframe_attention(q, k, v, ids, w.T, w.H, w.W, out=attn_out)
+        rf.rf_keyframe_attention_ws(q, k, v, ids, w.T, w.H, w.W, out=attn_out, workspace=ws)
         if ev is not None:
             ev[1].record()
         rf.rf_scatter_frames(attn_out, full_out, ids, w.T, w.N)
@@ -199,13 +203,13 @@ def main():
     if not args.no_comparator:
         all_out = torch.empty((w.S, w.heads, w.head_dim), dtype=q.dtype, device=dev)
         all_ids = list(range(w.T))
-        rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=all_out)
+        rf.rf_keyframe_attention_ws(q, k, v, all_ids, w.T, w.H, w.W, out=all_out, workspace=ws)
         torch.cuda.synchronize()
         n_all = max(1, min(args.steps, 5))
         ev_all = _events(n_all)
         for i in range(n_all):
             ev_all[i][0].record()
-            rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=all_out)
+            rf.rf_keyframe_attention_ws(q, k, v, all_ids, w.T, w.H, w.W, out=all_out, workspace=ws)
             ev_all[i][1].record()
         torch.cuda.synchronize()
         all_ms = _avg_ms(ev_all)
@@ -229,10 +233,10 @@ def main():
         result["rolling_cache"] = rolling_cache(w, args)
 
     if not args.no_frame_mask:
-        result["frame_mask"] = frame_mask(w, q, k, v, args)
+        result["frame_mask"] = frame_mask(w, q, k, v, ws, args)
 
     if not args.no_schedule:
-        result["schedule"] = schedule_loop(w, args)
+        result["schedule"] = schedule_loop(w, ws, args)
 
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
@@ -279,7 +283,7 @@ def selection(w, args):
             "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
 
 
-def frame_mask(w, q, k, v, args):
+def frame_mask(w, q, k, v, ws, args):
     """Keyframe-only attention (a frame-level key/value mask; Sec. 4's
     ablations): the keyframes' queries over the keyframes' keys only, timed
     like the main attention launch."""
@@ -287,13 +291,15 @@ def frame_mask(w, q, k, v, args):
     from paper_2606_06309_amd import accounting, binding as rf
 
     out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=q.dtype, device="cuda")
-    rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out)
+    need = rf.rf_attention_workspace(w.M, w.M, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype)
+    wsm = ws if ws.numel() >= need else torch.empty(need, dtype=torch.uint8, device="cuda")
+    rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out, workspace=wsm)
     torch.cuda.synchronize()
     n = max(3, args.steps)
     ev = _events(n)
     for a, b in ev:
         a.record()
-        rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out)
+        rf.rf_frame_attention(q, k, v, w.keyframes, w.keyframes, w.T, w.H, w.W, out=out, workspace=wsm)
         b.record()
     torch.cuda.synchronize()
     ms = _avg_ms(ev)
@@ -305,7 +311,7 @@ def frame_mask(w, q, k, v, args):
             "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop}
 
 
-def schedule_loop(w, args):
+def schedule_loop(w, ws, args):
     """A whole denoising schedule (Eq. 2, Alg. 2) at the workload's shape,
     attention path only: warm-up steps and Rhythmic Points run attention with
     every frame's queries; skipped steps project the non-keyframe latents
@@ -331,10 +337,10 @@ def schedule_loop(w, args):
         for i, step in enumerate(plan):
             q, k, v = sets[i % 2]
             if dense or step["phase"] != "skip":
-                rf.rf_keyframe_attention(q, k, v, all_ids, w.T, w.H, w.W, out=full_out)
+                rf.rf_keyframe_attention_ws(q, k, v, all_ids, w.T, w.H, w.W, out=full_out, workspace=ws)
             else:
                 rf.rf_project_latents(lat, (step["t_start"], step["t_end"], step["t"]), mask, out=proj)
-                rf.rf_keyframe_attention(q, k, v, ids, w.T, w.H, w.W, out=kq_out)
+                rf.rf_keyframe_attention_ws(q, k, v, ids, w.T, w.H, w.W, out=kq_out, workspace=ws)
                 rf.rf_scatter_frames(kq_out, full_out, ids, w.T, w.N)
 
     times = {}

@@ -162,6 +162,38 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
                           int32_t dtype, void *stream);
 
 /*
+ * rf_keyframe_attention with a caller workspace for a split-key tail: one
+ * bf16 workgroup of 256 query rows fills a compute unit, so ceil(M*N/256)*heads
+ * workgroups run in whole rounds of 256; the tiles beyond the last full round
+ * are cut along the keys into parts that run side by side, and a second small
+ * kernel combines each tile's parts (max of the parts' reference maxima,
+ * rescaled sums, one bf16 rounding). Rows of split tiles differ from the
+ * unsplit result only in fp32 summation order; which tiles are split depends
+ * on the launch's size, so the row-for-row bitwise identity between launches
+ * of different M that rf_keyframe_attention has does not hold here.
+ *
+ * workspace: device, 16-byte aligned, at least rf_attention_workspace bytes
+ *   (may be 0: then nothing is split), not overlapping q, k, v or out; its
+ *   contents are overwritten and meaningless afterwards. fp32 ignores it.
+ * Other arguments and errors as rf_keyframe_attention; RF_ERR_INVALID_ARG also
+ * for a NULL or too small workspace or an overlap.
+ */
+int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *out,
+                             const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                             int32_t heads, int32_t head_dim, int32_t dtype, void *workspace,
+                             int64_t workspace_bytes, void *stream);
+
+/*
+ * Bytes of workspace rf_keyframe_attention_ws (Mkv = T) or rf_frame_attention
+ * (Mkv key/value frames) uses for these sizes (host only; 0 when nothing is
+ * split, always 0 for RF_F32). The split assumes MI355X's 256 compute units.
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (T, M, Mkv),
+ * RF_ERR_UNSUPPORTED (head_dim, dtype).
+ */
+int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
+                           int32_t head_dim, int32_t dtype, int64_t *bytes_out);
+
+/*
  * Attention under a frame-level key/value mask: the frame mask M_Rhyme (in
  * the Discussions, a per-step frame mask that can be multiplied with a token
  * mask) with one key set for all query frames. The query rows are the tokens
@@ -176,13 +208,15 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
  * partly idle.
  *
  * kv_frames [Mkv]: strictly increasing, each in [0, T), 1 <= Mkv <= T (Mkv = T
- * is rf_keyframe_attention). All other arguments, layouts and errors as
- * rf_keyframe_attention (q_frames / Mq are its keyframe_ids / M).
+ * is rf_keyframe_attention). workspace / workspace_bytes: as
+ * rf_keyframe_attention_ws, or NULL for no split. All other arguments,
+ * layouts and errors as rf_keyframe_attention (q_frames / Mq are its
+ * keyframe_ids / M).
  */
 int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
                        const int32_t *q_frames, int32_t Mq, const int32_t *kv_frames, int32_t Mkv,
                        int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
-                       int32_t dtype, void *stream);
+                       int32_t dtype, void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * Frame gather: dst_compact[m*N + n] = src_full[frame_ids[m]*N + n] for rows

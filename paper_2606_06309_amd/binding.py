@@ -30,7 +30,8 @@ RF_MAX_FRAMES = 256
 EXPORTED = [
     "rf_status_string", "rf_last_error", "rf_abi_version",
     "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
-    "rf_project_latents", "rf_keyframe_attention", "rf_frame_attention",
+    "rf_project_latents", "rf_keyframe_attention", "rf_keyframe_attention_ws", "rf_attention_workspace",
+    "rf_frame_attention",
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
@@ -112,7 +113,12 @@ lib.rf_keyframe_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i3
                                       _i32, _i32, _i32, _vp]
 lib.rf_keyframe_attention.restype = ctypes.c_int
 lib.rf_frame_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32p, _i32, _i32, _i32, _i32,
-                                   _i32, _i32, _i32, _vp]
+                                   _i32, _i32, _i32, _vp, _i64, _vp]
+lib.rf_keyframe_attention_ws.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
+                                         _i32, _i32, _i32, _vp, _i64, _vp]
+lib.rf_keyframe_attention_ws.restype = ctypes.c_int
+lib.rf_attention_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64)]
+lib.rf_attention_workspace.restype = ctypes.c_int
 lib.rf_frame_attention.restype = ctypes.c_int
 lib.rf_gather_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
 lib.rf_gather_frames.restype = ctypes.c_int
@@ -282,9 +288,51 @@ def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=Non
     return out
 
 
-def rf_frame_attention(q, k, v, q_frames, kv_frames, T: int, H: int, W: int, out=None, stream=None):
+def rf_attention_workspace(M: int, Mkv: int, T: int, H: int, W: int, heads: int, head_dim: int, dtype) -> int:
+    """Bytes of split-tail workspace rf_keyframe_attention_ws (Mkv = T) or
+    rf_frame_attention uses (0: nothing is split)."""
+    n = _i64(0)
+    code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    _check(lib.rf_attention_workspace(M, Mkv, T, H, W, heads, head_dim, code, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _workspace(workspace, nbytes, device):
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def rf_keyframe_attention_ws(q, k, v, keyframe_ids, T: int, H: int, W: int, out=None, workspace=None,
+                             stream=None):
+    """rf_keyframe_attention with the split-key tail; the workspace (a device
+    tensor) is allocated here if not given."""
+    if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share a dtype")
+    S, heads, d = q.shape
+    if S != T * H * W:
+        raise ValueError(f"S = {S} differs from T*H*W = {T * H * W}")
+    ids, ids_p = _ids(keyframe_ids)
+    M = ids.size
+    if out is None:
+        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+    if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
+        raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
+    need = rf_attention_workspace(M, T, T, H, W, heads, d, q.dtype) if M > 0 else 0
+    workspace, wbytes = _workspace(workspace, need, q.device)
+    _check(lib.rf_keyframe_attention_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                        ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
+                                        _dev(workspace, "workspace"), wbytes, _stream(stream)))
+    return out
+
+
+def rf_frame_attention(q, k, v, q_frames, kv_frames, T: int, H: int, W: int, out=None, workspace=None,
+                       stream=None):
     """Attention of the tokens of q_frames over the keys/values of kv_frames
-    only; q, k, v [T*H*W][heads][head_dim] -> out [Mq*H*W][heads][head_dim]."""
+    only; q, k, v [T*H*W][heads][head_dim] -> out [Mq*H*W][heads][head_dim].
+    workspace: a device tensor for the split-key tail, or None (no split)."""
     if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
         raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
     if not (q.dtype == k.dtype == v.dtype):
@@ -299,9 +347,11 @@ def rf_frame_attention(q, k, v, q_frames, kv_frames, T: int, H: int, W: int, out
         out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
     if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
         raise ValueError("out must be [Mq*H*W][heads][head_dim] of q's dtype")
+    ws_p, wbytes = (None, 0) if workspace is None else (_dev(workspace, "workspace"),
+                                                        workspace.numel() * workspace.element_size())
     _check(lib.rf_frame_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                   ids_p, M, kv_p, kv.size, T, H, W, heads, d, _dtype_code(q.dtype),
-                                  _stream(stream)))
+                                  ws_p, wbytes, _stream(stream)))
     return out
 
 

@@ -191,9 +191,18 @@ int rf_project_latents(const void *latents, void *out, const double timesteps[3]
 }
 
 // Shared validation and launch of the two attention entry points.
+// Bytes of split-tail workspace a bf16 attention of these sizes uses (0 for fp32
+// or when nothing is split); the sizes must already be valid.
+static int64_t attention_ws_need(int32_t M, int32_t n_kv, int32_t T, int64_t N, int32_t heads, int32_t head_dim,
+                                 int32_t dtype) {
+    if (dtype != RF_BF16) return 0;
+    return rf::attention_split(static_cast<int64_t>(M) * N, heads, head_dim, N, N * T, n_kv).ws_bytes;
+}
+
 static int attention_call(const void *q, const void *k, const void *v, void *out, const int32_t *q_ids,
                           int32_t M, const int32_t *kv_ids, int32_t Mkv, int32_t T, int32_t H, int32_t W,
-                          int32_t heads, int32_t head_dim, int32_t dtype, void *stream, const char *fn) {
+                          int32_t heads, int32_t head_dim, int32_t dtype, void *ws, int64_t ws_bytes,
+                          void *stream, const char *fn) {
     if (!q || !k || !v || !out) return fail(RF_ERR_INVALID_ARG, "%s: NULL tensor", fn);
     if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
@@ -221,6 +230,19 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
     if (overlaps(out, out_bytes, q, in_bytes) || overlaps(out, out_bytes, k, in_bytes) ||
         overlaps(out, out_bytes, v, in_bytes))
         return fail(RF_ERR_INVALID_ARG, "%s: out overlaps q, k or v", fn);
+    const int32_t n_kv = (kv_ids && Mkv < T) ? Mkv : 0;
+    if (ws) {
+        const int64_t need = attention_ws_need(M, n_kv, T, N, heads, head_dim, dtype);
+        if (ws_bytes < need)
+            return fail(RF_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed", fn,
+                        static_cast<long long>(ws_bytes), static_cast<long long>(need));
+        if (!aligned16(ws)) return fail(RF_ERR_UNSUPPORTED, "%s: workspace must be 16-byte aligned", fn);
+        if (need > 0 && (overlaps(ws, need, q, in_bytes) || overlaps(ws, need, k, in_bytes) ||
+                         overlaps(ws, need, v, in_bytes) || overlaps(ws, need, out, out_bytes)))
+            return fail(RF_ERR_INVALID_ARG, "%s: workspace overlaps q, k, v or out", fn);
+        p.ws = need > 0 ? ws : nullptr;
+        p.ws_bytes = ws_bytes;
+    }
 
     p.q = q;
     p.k = k;
@@ -233,7 +255,7 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
     p.head_dim = head_dim;
     p.dtype = dtype;
     // every frame listed: the unmasked kernel
-    p.n_kv = (kv_ids && Mkv < T) ? Mkv : 0;
+    p.n_kv = n_kv;
     for (int32_t i = 0; i < p.n_kv; ++i) p.kvf[i] = kvf[i];
     return launched(rf::launch_attention(p, static_cast<hipStream_t>(stream)), fn);
 }
@@ -243,17 +265,42 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
                           int32_t W, int32_t heads, int32_t head_dim, int32_t dtype,
                           void *stream) {
     return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype,
-                          stream, "rf_keyframe_attention");
+                          nullptr, 0, stream, "rf_keyframe_attention");
+}
+
+int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *out,
+                             const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                             int32_t heads, int32_t head_dim, int32_t dtype, void *workspace,
+                             int64_t workspace_bytes, void *stream) {
+    const char *fn = "rf_keyframe_attention_ws";
+    if (!workspace) return fail(RF_ERR_INVALID_ARG, "%s: NULL workspace", fn);
+    return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype,
+                          workspace, workspace_bytes, stream, fn);
 }
 
 int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
                        const int32_t *q_frames, int32_t Mq, const int32_t *kv_frames, int32_t Mkv,
                        int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
-                       int32_t dtype, void *stream) {
+                       int32_t dtype, void *workspace, int64_t workspace_bytes, void *stream) {
     const char *fn = "rf_frame_attention";
     if (!kv_frames) return fail(RF_ERR_INVALID_ARG, "%s: kv_frames is NULL", fn);
     return attention_call(q, k, v, out, q_frames, Mq, kv_frames, Mkv, T, H, W, heads, head_dim, dtype,
-                          stream, fn);
+                          workspace, workspace_bytes, stream, fn);
+}
+
+int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
+                           int32_t head_dim, int32_t dtype, int64_t *bytes_out) {
+    const char *fn = "rf_attention_workspace";
+    if (!bytes_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    if (H <= 0 || W <= 0 || heads <= 0 || T <= 0 || M <= 0 || Mkv <= 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
+    if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
+    if (M > T || Mkv > T) return fail(RF_ERR_RANGE, "%s: M = %d or Mkv = %d exceeds T = %d", fn, M, Mkv, T);
+    if (head_dim != 64 && head_dim != 128)
+        return fail(RF_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
+    if (dtype != RF_BF16 && dtype != RF_F32) return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    *bytes_out = attention_ws_need(M, Mkv < T ? Mkv : 0, T, static_cast<int64_t>(H) * W, heads, head_dim, dtype);
+    return ok();
 }
 
 static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int32_t M, int32_t T,

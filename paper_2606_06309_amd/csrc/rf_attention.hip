@@ -36,6 +36,12 @@
 //    8 XCDs, so tile = (id % 8) * per_xcd + id / 8 gives each XCD a contiguous,
 //    head-major range of tiles and the workgroups resident on one XCD stream
 //    the same head's K/V through that XCD's L2.
+//  * Split-key tail (when the caller provides a workspace): one workgroup
+//    fills a CU, so a launch of n tiles runs in ceil(n / 256) rounds and the
+//    last round may leave most CUs idle. The tiles beyond the last full round
+//    are then split along the keys into parts that run as extra workgroups;
+//    each part writes its unnormalised (O, m, l) in fp32, and a small kernel
+//    combines the parts of a tile (max of the references, rescaled sums).
 #include "rf_internal.h"
 
 namespace rf {
@@ -46,6 +52,8 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // Data moves as 32-bit words; bf16 vectors are only ever formed by a
 // whole-vector bitcast of a u32x4 (or of one scalar word) right before the
@@ -76,6 +84,12 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
 constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
 constexpr int kXcds = 8;
+// Split-key tail: compute units a round of whole tiles fills (one workgroup
+// per CU on MI355X), the most parts a tail tile is cut into, and the fewest
+// key tiles a part may have.
+constexpr int kSplitCUs = 256;
+constexpr int kMaxSplit = 8;
+constexpr int kMinKvPerSplit = 8;
 constexpr float kRebaseBound = RF_ATTN_REBASE_BOUND;   // largest tile row sum kept without a rebase
 static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
 
@@ -89,8 +103,13 @@ struct AttnKArgs {
     int64_t Mq;
     int32_t heads;
     int32_t n_qtiles;
-    int32_t total_tiles;
+    int32_t total_tiles;    // tiles computed whole (all tiles when there is no split)
     int32_t per_xcd;
+    int32_t grid_direct;    // workgroups of the whole tiles (per_xcd * 8)
+    int32_t split;          // parts per tail tile (0: no split)
+    int32_t kv_per_split;   // key tiles per part
+    float *ws_o;            // [tail tile * split + part][kBr][D] unnormalised O
+    float *ws_ml;           // [tail tile * split + part][kBr][2] reference max (log2 domain), row sum
     float scale_log2;   // log2(e) / sqrt(d)
     int32_t kf[kMaxFrames];
     // key/value frame list (frame-masked form only): the keys are the tokens
@@ -278,8 +297,17 @@ void attn_bf16_kernel(const AttnKArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t v0[L::kTileBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v1[L::kTileBytes];
 
-    const int tile = static_cast<int>(blockIdx.x % kXcds) * a.per_xcd + static_cast<int>(blockIdx.x / kXcds);
-    if (tile >= a.total_tiles) return;
+    const int bid = blockIdx.x;
+    int tile, part = -1;
+    if (bid < a.grid_direct) {
+        tile = (bid % kXcds) * a.per_xcd + bid / kXcds;
+        if (tile >= a.total_tiles) return;
+    } else {   // a part of a tail tile (tail tiles follow the whole ones in tile order)
+        const int u = bid - a.grid_direct;
+        const int tt = u / a.split;
+        part = u - tt * a.split;
+        tile = a.total_tiles + tt;
+    }
     const int head = tile / a.n_qtiles;
     const int qt = tile - head * a.n_qtiles;
     const int tid = threadIdx.x;
@@ -451,19 +479,24 @@ void attn_bf16_kernel(const AttnKArgs a) {
     };
 
     const int64_t ntiles = kKvList ? static_cast<int64_t>(a.n_kv) * a.tiles_per_frame : (a.S + kBc - 1) / kBc;
-    Geom cur = geom(0);
+    int64_t t_begin = 0, t_end = ntiles;
+    if (part >= 0) {
+        t_begin = static_cast<int64_t>(part) * a.kv_per_split;
+        t_end = t_begin + a.kv_per_split < ntiles ? t_begin + a.kv_per_split : ntiles;
+    }
+    Geom cur = geom(t_begin);
     issue(cur, k0, v0);
     tile_done();
-    for (int64_t t = 0; t < ntiles; t += 2) {
+    for (int64_t t = t_begin; t < t_end; t += 2) {
         Geom nxt = cur;
-        if (t + 1 < ntiles) {
+        if (t + 1 < t_end) {
             nxt = geom(t + 1);
             issue(nxt, k1, v1);
         }
         compute(cur.valid, k0, v0);
         tile_done();
-        if (t + 1 >= ntiles) break;
-        if (t + 2 < ntiles) {
+        if (t + 1 >= t_end) break;
+        if (t + 2 < t_end) {
             cur = geom(t + 2);
             issue(cur, k0, v0);
         }
@@ -471,8 +504,27 @@ void attn_bf16_kernel(const AttnKArgs a) {
         tile_done();
     }
 
-    // ---- epilogue: normalise, round to bf16, store the compact row ----
     l_run = halves_sum(l_run);
+    if (part >= 0) {
+        // ---- a part of a tail tile: unnormalised O and (m, l) for the combine kernel ----
+        if (row < a.Mq) {
+            const int64_t slot = static_cast<int64_t>(tile - a.total_tiles) * a.split + part;
+            const int64_t r = slot * kBr + wave * 32 + col;
+            float *po = a.ws_o + r * D;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4) {
+                    const int rr = g4 * 4;
+                    *reinterpret_cast<f32x4_t *>(po + db * 32 + g4 * 8 + grp * 4) =
+                        f32x4_t{oacc[db][rr], oacc[db][rr + 1], oacc[db][rr + 2], oacc[db][rr + 3]};
+                }
+            if (grp == 0) *reinterpret_cast<f32x2_t *>(a.ws_ml + r * 2) = f32x2_t{m_run, l_run};
+        }
+        return;
+    }
+
+    // ---- epilogue: normalise, round to bf16, store the compact row ----
     if (row < a.Mq) {
         const float inv = 1.0f / l_run;
         uint16_t *op = a.out + row * rs + static_cast<int64_t>(head) * D;
@@ -487,6 +539,65 @@ void attn_bf16_kernel(const AttnKArgs a) {
                 *reinterpret_cast<u32x2_t *>(op + db * 32 + g4 * 8 + grp * 4) = w;
             }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Combine of the split tail: for each row of a tail tile, the parts' reference
+// maxima m_p (log2 domain), row sums l_p and unnormalised outputs O_p give
+//   m = max_p m_p,  out = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p,
+// rounded to bf16. Each thread owns 8 output dimensions of one row.
+// ---------------------------------------------------------------------------
+
+struct CombineArgs {
+    const float *ws_o;
+    const float *ws_ml;
+    uint16_t *out;
+    int64_t Mq;
+    int32_t heads;
+    int32_t n_qtiles;
+    int32_t first_tail;   // tile index of the first tail tile
+    int32_t split;
+};
+
+constexpr int kCombineThreads = 256;
+
+template <int D>
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(const CombineArgs a) {
+    constexpr int kTpr = D / 8;                       // threads per row
+    constexpr int kRows = kCombineThreads / kTpr;     // rows per workgroup
+    constexpr int kGroups = kBr / kRows;              // workgroups per tail tile
+    const int tt = blockIdx.x / kGroups;
+    const int r = (blockIdx.x - tt * kGroups) * kRows + threadIdx.x / kTpr;
+    const int c8 = threadIdx.x % kTpr;
+    const int tile = a.first_tail + tt;
+    const int head = tile / a.n_qtiles;
+    const int qt = tile - head * a.n_qtiles;
+    const int64_t row = static_cast<int64_t>(qt) * kBr + r;
+    if (row >= a.Mq) return;
+    const int64_t base = static_cast<int64_t>(tt) * a.split * kBr + r;   // slot of part 0 of this row
+    float m = -__builtin_huge_valf();
+    for (int p = 0; p < a.split; ++p) m = fmaxf(m, a.ws_ml[(base + static_cast<int64_t>(p) * kBr) * 2]);
+    float l = 0.0f, o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = 0.0f;
+    for (int p = 0; p < a.split; ++p) {
+        const int64_t slot = base + static_cast<int64_t>(p) * kBr;
+        const f32x2_t ml = *reinterpret_cast<const f32x2_t *>(a.ws_ml + slot * 2);
+        const float wgt = fast_exp2(ml[0] - m);
+        l = fmaf(wgt, ml[1], l);
+        const f32x4_t *po = reinterpret_cast<const f32x4_t *>(a.ws_o + slot * D + c8 * 8);
+        const f32x4_t x0 = po[0], x1 = po[1];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            o[e] = fmaf(wgt, x0[e], o[e]);
+            o[e + 4] = fmaf(wgt, x1[e], o[e + 4]);
+        }
+    }
+    const float inv = 1.0f / l;
+    const int64_t rs = static_cast<int64_t>(a.heads) * D;
+    const u32x4_t w = {pack_bf16x2(o[0] * inv, o[1] * inv), pack_bf16x2(o[2] * inv, o[3] * inv),
+                       pack_bf16x2(o[4] * inv, o[5] * inv), pack_bf16x2(o[6] * inv, o[7] * inv)};
+    *reinterpret_cast<u32x4_t *>(a.out + row * rs + static_cast<int64_t>(head) * D + c8 * 8) = w;
 }
 
 // ---------------------------------------------------------------------------
@@ -589,6 +700,32 @@ __global__ __launch_bounds__(2 * kF32Rows) void attn_f32_kernel(const AttnF32Arg
 
 }  // namespace
 
+AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv) {
+    AttnSplit sp{};
+    const int64_t total = (Mq + kBr - 1) / kBr * heads;
+    const int64_t kv_tiles = n_kv > 0 ? static_cast<int64_t>(n_kv) * ((N + kBc - 1) / kBc) : (S + kBc - 1) / kBc;
+    const int64_t tail = total % kSplitCUs;
+    sp.n_direct = total;
+    if (tail == 0) return sp;
+    // tail time in rounds of whole tiles for s parts: ceil(tail * s / CUs) / s
+    int best_s = 1;
+    double best = 1.0;
+    for (int s = 2; s <= kMaxSplit && kv_tiles / s >= kMinKvPerSplit; ++s) {
+        const double cost = static_cast<double>((tail * s + kSplitCUs - 1) / kSplitCUs) / s;
+        if (cost < best - 1e-9) {
+            best = cost;
+            best_s = s;
+        }
+    }
+    if (best_s == 1) return sp;
+    sp.n_direct = total - tail;
+    sp.n_tail = tail;
+    sp.split = best_s;
+    sp.kv_per_split = (kv_tiles + best_s - 1) / best_s;
+    sp.ws_bytes = tail * best_s * kBr * (static_cast<int64_t>(head_dim) * 4 + 8);
+    return sp;
+}
+
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
     const int64_t Mq = static_cast<int64_t>(p.M) * p.N;
     if (p.dtype == RF_BF16) {
@@ -602,14 +739,28 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         a.Mq = Mq;
         a.heads = p.heads;
         const int64_t nq = (Mq + kBr - 1) / kBr;
-        const int64_t total = nq * p.heads;
+        AttnSplit sp{};
+        sp.n_direct = nq * p.heads;
+        if (p.ws) {
+            sp = attention_split(Mq, p.heads, p.head_dim, p.N, p.S, p.n_kv);
+            if (sp.split > 0 && p.ws_bytes < sp.ws_bytes) return hipErrorInvalidValue;
+        }
+        const int64_t total = sp.n_direct;
         const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-        if (total > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
+        if (nq * p.heads > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
         // per-lane load offsets inside a tile are 32-bit: kBc token rows must span < 2 GiB
         if (static_cast<int64_t>(p.heads) * p.head_dim * 2 * kBc >= 0x7fffffffLL) return hipErrorInvalidConfiguration;
         a.n_qtiles = static_cast<int32_t>(nq);
         a.total_tiles = static_cast<int32_t>(total);
         a.per_xcd = static_cast<int32_t>(per_xcd);
+        a.grid_direct = static_cast<int32_t>(per_xcd * kXcds);
+        a.split = static_cast<int32_t>(sp.split);
+        a.kv_per_split = static_cast<int32_t>(sp.kv_per_split);
+        const int64_t n_parts = sp.n_tail * sp.split;
+        if (sp.split > 0) {
+            a.ws_o = static_cast<float *>(p.ws);
+            a.ws_ml = a.ws_o + n_parts * kBr * p.head_dim;
+        }
         a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(p.head_dim)));
         for (int i = 0; i < p.M; ++i) a.kf[i] = p.kf[i];
         a.n_kv = p.n_kv;
@@ -617,7 +768,7 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         for (int i = 0; i < p.n_kv; ++i) a.kvf[i] = p.kvf[i];
         if (p.n_kv > 0 && static_cast<int64_t>(p.n_kv) * a.tiles_per_frame > 0x7fffffffLL)
             return hipErrorInvalidConfiguration;
-        const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds)), block(kThreads);
+        const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds + n_parts)), block(kThreads);
         if (p.n_kv > 0) {
             if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
             else hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);
@@ -625,6 +776,22 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
             if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, stream, a);
             else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, stream, a);
         }
+        if (sp.split == 0) return hipGetLastError();
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        CombineArgs c{};
+        c.ws_o = a.ws_o;
+        c.ws_ml = a.ws_ml;
+        c.out = a.out;
+        c.Mq = Mq;
+        c.heads = p.heads;
+        c.n_qtiles = a.n_qtiles;
+        c.first_tail = a.total_tiles;
+        c.split = a.split;
+        const int rows_per_wg = kCombineThreads / (p.head_dim / 8);
+        const dim3 cgrid(static_cast<uint32_t>(sp.n_tail * (kBr / rows_per_wg))), cblock(kCombineThreads);
+        if (p.head_dim == 128) hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, cblock, 0, stream, c);
+        else hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, cblock, 0, stream, c);
         return hipGetLastError();
     }
     AttnF32Args a{};

@@ -28,7 +28,23 @@ struct AttnParams {
     // 0: keys are all S tokens; > 0: only the tokens of frames kvf[0..n_kv)
     int32_t n_kv;
     int32_t kvf[kMaxFrames];
+    // optional workspace for the split-key tail (NULL: no split)
+    void *ws;
+    int64_t ws_bytes;
 };
+
+// How the bf16 attention of Mq query rows is cut: n_direct whole tiles, then
+// n_tail tiles split into `split` parts of kv_per_split key tiles (split = 0:
+// no split), needing ws_bytes of workspace.
+struct AttnSplit {
+    int64_t n_direct;
+    int64_t n_tail;
+    int64_t split;
+    int64_t kv_per_split;
+    int64_t ws_bytes;
+};
+
+AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv);
 
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream);
 

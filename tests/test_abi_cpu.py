@@ -146,7 +146,7 @@ def _fattn(q=A, k=B_, v=C_, out=O_, ids=(0, 2, 4), kv=(0, 2, 4), T=5, H=8, W=8, 
     arr = (ctypes.c_int32 * max(1, len(ids)))(*ids)
     kva = (ctypes.c_int32 * max(1, len(kv)))(*kv) if kv is not None else None
     return lib.rf_frame_attention(q, k, v, out, arr, len(ids), kva, 0 if kv is None else len(kv), T, H, W,
-                                  heads, d, dtype, None)
+                                  heads, d, dtype, None, 0, None)
 
 
 @pytest.mark.parametrize("kwargs,status", [
@@ -164,6 +164,43 @@ def _fattn(q=A, k=B_, v=C_, out=O_, ids=(0, 2, 4), kv=(0, 2, 4), T=5, H=8, W=8, 
 def test_frame_attention_validation(kwargs, status):
     assert _fattn(**kwargs) == status
     assert lib.rf_last_error().decode().startswith("rf_frame_attention")
+
+
+def test_attention_workspace_sizes():
+    # 2,712 tiles of 256 rows at 33 x 45 x 80, 24 heads: 152 beyond 10 rounds, split in 5
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16) == 152 * 5 * 256 * (128 * 4 + 8)
+    # 40 heads, 6 keyframes of 45 x 80: 3,400 tiles, 72 beyond 13 rounds, split in 7
+    assert rf.rf_attention_workspace(6, 21, 21, 45, 80, 40, 128, rf.RF_BF16) == 72 * 7 * 256 * 520
+    # whole rounds need nothing; fp32 never splits; too few key tiles to split
+    assert rf.rf_attention_workspace(8, 33, 33, 48, 64, 24, 128, rf.RF_BF16) == 0
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_F32) == 0
+    assert rf.rf_attention_workspace(3, 5, 5, 8, 8, 2, 64, rf.RF_BF16) == 0
+    n = ctypes.c_int64(0)
+    for args, status in [((0, 5, 5, 8, 8, 2, 64, 0), rf.RF_ERR_INVALID_ARG),
+                         ((6, 5, 5, 8, 8, 2, 64, 0), rf.RF_ERR_RANGE),
+                         ((2, 5, 5, 8, 8, 2, 96, 0), rf.RF_ERR_UNSUPPORTED),
+                         ((2, 5, 300, 8, 8, 2, 64, 0), rf.RF_ERR_RANGE)]:
+        assert lib.rf_attention_workspace(*args, ctypes.byref(n)) == status
+    assert lib.rf_attention_workspace(2, 5, 5, 8, 8, 2, 64, 0, None) == rf.RF_ERR_INVALID_ARG
+
+
+def _attn_ws(ws=0x50000000, ws_bytes=1 << 30, T=8, H=16, W=16, heads=2, d=128, ids=(0, 5), out=O_):
+    arr = (ctypes.c_int32 * len(ids))(*ids)
+    return lib.rf_keyframe_attention_ws(A, B_, C_, out, arr, len(ids), T, H, W, heads, d, rf.RF_BF16,
+                                        ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(ws=0), rf.RF_ERR_INVALID_ARG),
+    (dict(ws_bytes=1000), rf.RF_ERR_INVALID_ARG),
+    (dict(ws=0x50000008), rf.RF_ERR_UNSUPPORTED),
+    (dict(ws=A + 64), rf.RF_ERR_INVALID_ARG),          # workspace inside q
+    (dict(ws=O_ - 64), rf.RF_ERR_INVALID_ARG),         # workspace running into out
+])
+def test_attention_ws_validation(kwargs, status):
+    assert rf.rf_attention_workspace(2, 8, 8, 16, 16, 2, 128, rf.RF_BF16) > 0
+    assert _attn_ws(**kwargs) == status
+    assert lib.rf_last_error().decode().startswith("rf_keyframe_attention_ws")
 
 
 def _proj(lat=A, out=B_, ts=(24.0, 21.0, 23.0), mask=(1, 0, 1, 0, 1), B=1, C=4, T=5, Hl=16,

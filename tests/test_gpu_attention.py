@@ -204,3 +204,88 @@ def test_fp32_path_head_dim_128():
     w = workloads.custom(3, 8, 9, 2, 128, (0, 2), dtype="f32", seed=36)
     got, ref, _ = _run_case(w)
     assert_parity(got, ref, "f32", "f32 d=128")
+
+
+# --- split-key tail (rf_keyframe_attention_ws) ---------------------------------------
+
+SPLIT_CASES = [
+    # every tile in the tail: 4 tiles, 32 key tiles -> 4 parts
+    workloads.custom(8, 16, 16, 2, 128, (0, 5), dtype="bf16", seed=51),
+    # ragged: 390 query rows (2 tiles per head, the second partial), 19 key tiles -> 2 parts
+    workloads.custom(9, 10, 13, 3, 128, (0, 4, 8), dtype="bf16", seed=52),
+    workloads.custom(9, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=53),
+    # 3 frames of 40 x 52: 6,240 rows, 25 tiles per head, 4 heads -> 100 tiles, 98 key tiles -> 5 parts
+    workloads.custom(3, 40, 52, 4, 128, (0, 1, 2), dtype="bf16", seed=54),
+]
+
+
+def _split_plan(w):
+    return rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, w.torch_dtype)
+
+
+@pytest.mark.parametrize("w", SPLIT_CASES, ids=lambda w: f"T{w.T}_N{w.N}_h{w.heads}_d{w.head_dim}")
+def test_split_tail_every_element(w):
+    assert _split_plan(w) > 0, "case must exercise the split"
+    print(f"[case] split tail {w.name} T={w.T} N={w.N} heads={w.heads} d={w.head_dim}", flush=True)
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    ws = torch.full((_split_plan(w),), 0x7f, dtype=torch.uint8, device="cuda")   # NaN-patterned garbage
+    out = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.keyframe_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, w.N)
+    assert_parity(_to_f64(out), ref, "bf16", f"split {w.name}")
+    # and against the unsplit kernel: the same values up to fp32 summation order
+    plain = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    assert np.abs(_to_f64(out) - _to_f64(plain)).max() <= 2.0 ** -7 * max(1.0, np.abs(ref).max())
+
+
+def test_split_tail_deterministic_and_reusable_workspace():
+    w = SPLIT_CASES[1]
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    ws = torch.empty((_split_plan(w),), dtype=torch.uint8, device="cuda")
+    a = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, workspace=ws)
+    b = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_split_tail_long_workload():
+    """33 frames of 45 x 80, 24 heads: 2,712 tiles = 10 full rounds + 152 tiles
+    split in 5. Whole tiles are bit-identical to the unsplit kernel (same code
+    path); sampled rows of the split tiles (heads 22 and 23) and of whole tiles
+    against the oracle."""
+    w = workloads.WORKLOADS["long"]
+    need = _split_plan(w)
+    assert need == 152 * 5 * 256 * (128 * 4 + 8)
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
+    out = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, workspace=ws)
+    plain = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    n_qt = -(-w.M * w.N // 256)
+    first_tail = 2560
+    # whole tiles: every (head, q-tile) below first_tail
+    o4 = out.view(w.M * w.N, w.heads, w.head_dim)
+    p4 = plain.view(w.M * w.N, w.heads, w.head_dim)
+    for h in range(w.heads):
+        rows_whole = min(w.M * w.N, max(0, first_tail - h * n_qt) * 256)
+        if rows_whole:
+            assert torch.equal(o4[:rows_whole, h], p4[:rows_whole, h]), h
+    rows = workloads.sample_rows(w, per_head=24)
+    heads = np.array([0, 22, 23])
+    got = _to_f64(out[torch.as_tensor(rows, device="cuda")])[:, heads]
+    ref = oracle.keyframe_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, w.N, rows=rows, heads=heads)
+    assert_parity(got, ref, "bf16", "long split tail")
+
+
+def test_frame_attention_split_tail():
+    w = workloads.custom(12, 16, 16, 2, 128, (0, 4, 8), dtype="bf16", seed=55)
+    kvf = (0, 1, 2, 4, 5, 7, 8, 9, 10, 11)    # 40 key tiles
+    need = rf.rf_attention_workspace(w.M, len(kvf), w.T, w.H, w.W, w.heads, w.head_dim, w.torch_dtype)
+    assert need > 0
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
+    out = rf.rf_frame_attention(q, k, v, w.keyframes, kvf, w.T, w.H, w.W, workspace=ws)
+    torch.cuda.synchronize()
+    ref = oracle.frame_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, kvf, w.N)
+    assert_parity(_to_f64(out), ref, "bf16", "frame mask split tail")
