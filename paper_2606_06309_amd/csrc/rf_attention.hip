@@ -435,8 +435,10 @@ void attn_bf16_kernel(const AttnKArgs a) {
         auto probs = [&]() {
             // probabilities, packed as the B operand of O^T = V^T P^T:
             // operand c takes accumulators 8*(c%2) .. 8*(c%2)+7 of block c/2.
-            // The row sum adds the bf16-rounded values the matrix core consumes.
-            float ls = 0.0f;
+            // The row sum adds the bf16-rounded values the matrix core consumes,
+            // in four independent partial sums (a single chain of dependent adds
+            // would hold up the end of the softmax).
+            float lsp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int b = 0; b < kNB; ++b)
 #pragma unroll
@@ -444,10 +446,10 @@ void attn_bf16_kernel(const AttnKArgs a) {
                     const float p0 = fast_exp2(fmaf(sacc[b][r], sl2, -m_run));
                     const float p1 = fast_exp2(fmaf(sacc[b][r + 1], sl2, -m_run));
                     const uint32_t word = pack_bf16x2(p0, p1);
-                    ls = add_bf16x2(word, ls);
+                    lsp[(r / 2) % 4] = add_bf16x2(word, lsp[(r / 2) % 4]);
                     pw[b * 2 + r / 8][(r % 8) / 2] = word;
                 }
-            return ls;
+            return ((lsp[0] + lsp[1]) + lsp[2]) + lsp[3];
         };
         float ls = probs();
         // decided per query row (its two lanes agree), so a row's result depends on
