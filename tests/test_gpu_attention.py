@@ -25,11 +25,14 @@ def _to_f64(t):
     return torch_bf16_to_f64(t) if t.dtype == torch.bfloat16 else t.detach().cpu().double().numpy()
 
 
-def _run_case(w, scale=None, rows=None, heads=None, seed=None):
+def _run_case(w, scale=None, rows=None, heads=None, seed=None, split=False):
     print(f"[case] {w.name} T={w.T} H={w.H} W={w.W} heads={w.heads} d={w.head_dim} "
-          f"kf={w.keyframes} dtype={w.dtype}", flush=True)
+          f"kf={w.keyframes} dtype={w.dtype} split={split}", flush=True)
     q, k, v = workloads.make_qkv(w, device="cuda", scale=scale, seed=seed)
-    out = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
+    if split:
+        out = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W)
+    else:
+        out = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
     torch.cuda.synchronize()
     qh, kh, vh = q.cpu(), k.cpu(), v.cpu()
     ref = oracle.keyframe_attention(qh, kh, vh, w.keyframes, w.N, rows=rows, heads=heads)
@@ -181,22 +184,30 @@ def test_two_streams_are_ordered():
 
 # --- the workloads at full size, sampled rows -------------------------------------------
 
+@pytest.mark.parametrize("split", [False, True], ids=["whole", "split"])
 @pytest.mark.parametrize("name", ["small", "480p", "720p", "long"])
-def test_workload_sampled_rows(name):
+def test_workload_sampled_rows(name, split):
     w = workloads.WORKLOADS[name]
     rows = workloads.sample_rows(w, per_head=24 if w.heads > 12 else 48)
-    got, ref, _ = _run_case(w, rows=rows)
+    got, ref, _ = _run_case(w, rows=rows, split=split)
     st = assert_parity(got, ref, "bf16", name)
     print(f"[parity] {name}: {st}", flush=True)
 
 
-def test_all_frame_comparator_sampled_rows():
+@pytest.mark.parametrize("split", [False, True], ids=["whole", "split"])
+def test_all_frame_comparator_sampled_rows(split):
+    """All 33 frames as queries at 45 x 80, 24 heads (11,160 tiles; with the
+    split, the last 152 tiles of head 23 run in parts): sampled rows, among
+    them rows of head 23's last tiles."""
     base = workloads.WORKLOADS["long"]
     w = workloads.Workload("long-all", base.index, base.T, base.H, base.W, base.heads,
                            base.head_dim, base.dtype, tuple(range(base.T)), base.qkv_scale,
                            base.latent_c, base.latent_hw)
-    rows = np.sort(np.random.default_rng(9).choice(w.M * w.N, 16, replace=False))
-    got, ref, _ = _run_case(w, rows=rows, heads=[0, 11, 23])
+    rng = np.random.default_rng(9)
+    rows = np.unique(np.concatenate([rng.choice(w.M * w.N, 12, replace=False),
+                                     rng.choice(np.arange(313 * 256, w.M * w.N), 6, replace=False),
+                                     [w.M * w.N - 1]]))
+    got, ref, _ = _run_case(w, rows=rows, heads=[0, 11, 23], split=split)
     assert_parity(got, ref, "bf16", "long all-frame")
 
 
