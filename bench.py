@@ -89,7 +89,16 @@ def cpu_baseline(w, q, k, v, target_s):
     n = int(max(n0, min(200000, n0 * target_s / max(t_cal, 1e-3))))
     t = run(n)
     flop = n * accounting.attention_flops(1, w.S, w.head_dim, 1)
-    return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle", "cpu": cpu,
             "sample": f"{n} random (keyframe row, head) pairs of the {w.name} workload, each over "
                       f"all S={w.S} keys, fp64; {t:.1f} s"}
 
