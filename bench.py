@@ -103,22 +103,33 @@ def cpu_baseline(w, q, k, v, target_s):
                       f"all S={w.S} keys, fp64; {t:.1f} s"}
 
 
+def source_digest(path):
+    """sha256 of a source file's code: comments removed and whitespace
+    collapsed, so that edits of comments alone keep the digest."""
+    import hashlib
+    import re
+    text = open(path, encoding="utf-8").read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = " ".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()
+
+
 def profiled_traffic(workload):
     """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary, or None when there is none or the attention source has changed
+    summary, or None when there is none or the attention code has changed
     since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"attn_bf16_{workload}_traffic.txt")
     src = os.path.join(ROOT, "paper_2606_06309_amd", "csrc", "rf_attention.hip")
     if not os.path.exists(path):
         return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    sha = source_digest(src)
     fields = {}
     for line in open(path):
         if ":" in line:
             key, _, val = line.partition(":")
             fields[key.strip()] = val.strip()
-    if fields.get("attention source sha256") != sha:
+    if fields.get("attention code sha256") != sha:
         return None
     try:
         return int(fields["traffic_bytes_per_launch"])

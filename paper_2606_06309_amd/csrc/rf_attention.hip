@@ -42,6 +42,10 @@
 //    are then split along the keys into parts that run as extra workgroups;
 //    each part writes its unnormalised (O, m, l) in fp32, and a small kernel
 //    combines the parts of a tile (max of the references, rescaled sums).
+//  * Frame-level key/value mask (the kKvList form): the key loop walks a list
+//    of frames in 64-key tiles that never cross a frame; masked frames are
+//    never read.
+// The fp32 kernel at the end is a plain correctness path (fp32 throughout).
 #include "rf_internal.h"
 
 namespace rf {
