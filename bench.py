@@ -89,6 +89,12 @@ def cpu_baseline(w, q, k, v, target_s):
     n = int(max(n0, min(200000, n0 * target_s / max(t_cal, 1e-3))))
     t = run(n)
     flop = n * accounting.attention_flops(1, w.S, w.head_dim, 1)
+    # the same oracle on one thread, a short sample (about a fifth of the budget)
+    oracle.set_num_threads(1)
+    n1 = max(1, int(n / max(1, cores) * 0.2))
+    t1 = run(n1)
+    oracle.set_num_threads(cores)
+    flop1 = n1 * accounting.attention_flops(1, w.S, w.head_dim, 1)
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -99,6 +105,7 @@ def cpu_baseline(w, q, k, v, target_s):
     except OSError:
         pass
     return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle", "cpu": cpu,
+            "one_thread": {"value": flop1 / t1 / 1e12, "sample": f"{n1} pairs, {t1:.1f} s"},
             "sample": f"{n} random (keyframe row, head) pairs of the {w.name} workload, each over "
                       f"all S={w.S} keys, fp64; {t:.1f} s"}
 

@@ -70,6 +70,8 @@ def _load():
         lib.orc_frame_cosine.restype = ctypes.c_int
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
+        lib.orc_set_num_threads.argtypes = [ctypes.c_int]
+        lib.orc_set_num_threads.restype = None
         _lib = lib
     return _lib
 
@@ -77,6 +79,11 @@ def _load():
 def num_threads() -> int:
     """Threads the C oracle's OpenMP loops use."""
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the C oracle's later OpenMP loops (for timing it)."""
+    _load().orc_set_num_threads(int(n))
 
 
 # ---------------------------------------------------------------------------

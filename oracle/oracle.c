@@ -47,6 +47,16 @@ int orc_num_threads(void)
 #endif
 }
 
+/* Threads of later parallel loops started from the calling thread (timing only). */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Scaled dot-product attention for a list of (query token, head) pairs.
  *
