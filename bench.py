@@ -340,12 +340,18 @@ def frame_mask(w, q, k, v, ws, args):
 
 def schedule_loop(w, ws, args):
     """A whole denoising schedule (Eq. 2, Alg. 2) at the workload's shape,
-    attention path only: warm-up steps and Rhythmic Points run attention with
-    every frame's queries; skipped steps project the non-keyframe latents
-    (Eq. 3, with the plan's interval and time) and run keyframe-query
-    attention plus the scatter. Q/K/V alternate between two seeded sets. The
-    same number of all-frame attention launches is timed as the dense
-    reference; `ideal` is the FLOP ratio of the plan."""
+    attention path only, three ways on the same plan:
+      latent: warm-up steps and Rhythmic Points run attention with every
+        frame's queries; skipped steps project the non-keyframe latents
+        (Eq. 3, the plan's interval and time) and run keyframe-query
+        attention plus the scatter;
+      cache: as latent, but the skipped steps take the non-keyframes' keys
+        and values from the per-layer rolling cache (App. B.2): initialised
+        from the last warm-up step's output, shift-and-store at each Rhythmic
+        Point, projection into K and V before each keyframe-query attention;
+      dense: every step all-frame attention (the reference).
+    Q/K/V alternate between two seeded sets. `ideal_flop_ratio` is the FLOP
+    ratio of the plan."""
     import torch
     from paper_2606_06309_amd import accounting, binding as rf, workloads
 
@@ -353,40 +359,60 @@ def schedule_loop(w, ws, args):
     plan = rf.rf_async_schedule(T_steps, T_w, T_mid, n_s, n_l)
     ids, mask = rf.rf_select_keyframes(w.keyframes, w.T)
     all_ids = list(range(w.T))
+    nonkey = [f for f in all_ids if f not in set(ids.tolist())]
     sets = [workloads.make_qkv(w, device="cuda", seed=900 + i) for i in range(2)]
     lat = workloads.make_latents(w, B=1, device="cuda")
     Hl, Wl = w.latent_hw
     proj = torch.empty((1, w.latent_c, w.T, Hl, Wl), dtype=lat.dtype, device="cuda")
-    kq_out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=sets[0][0].dtype, device="cuda")
-    full_out = torch.empty((w.S, w.heads, w.head_dim), dtype=sets[0][0].dtype, device="cuda")
+    dt = sets[0][0].dtype
+    kq_out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=dt, device="cuda")
+    full_out = torch.empty((w.S, w.heads, w.head_dim), dtype=dt, device="cuda")
+    D = w.heads * w.head_dim
+    el = torch.tensor([], dtype=dt).element_size()
+    store = torch.empty(rf.rf_cache_store_bytes(len(nonkey), w.N, D, dt) // el, dtype=dt, device="cuda") \
+        if nonkey else None
 
-    def run(dense):
+    def run(mode):
+        cache = None
         for i, step in enumerate(plan):
             q, k, v = sets[i % 2]
-            if dense or step["phase"] != "skip":
+            if mode == "dense" or step["phase"] != "skip":
                 rf.rf_keyframe_attention_ws(q, k, v, all_ids, w.T, w.H, w.W, out=full_out, workspace=ws)
+                if mode == "cache" and nonkey:
+                    if cache is None:
+                        if step["phase"] == "warmup" and i + 1 < len(plan) and plan[i + 1]["phase"] == "warmup":
+                            continue
+                        cache = rf.rf_cache_init(nonkey, w.T, w.N, D, dt, float(step["t"]), store=store,
+                                                 h_full=full_out)
+                    elif step["phase"] == "rhythmic":
+                        rf.rf_cache_shift_store(cache, float(step["t"]), store=store, h_full=full_out)
             else:
-                rf.rf_project_latents(lat, (step["t_start"], step["t_end"], step["t"]), mask, out=proj)
+                if mode == "cache" and cache is not None:
+                    rf.rf_cache_project_kv(cache, store, k, v, float(step["t"]))
+                else:
+                    rf.rf_project_latents(lat, (step["t_start"], step["t_end"], step["t"]), mask, out=proj)
                 rf.rf_keyframe_attention_ws(q, k, v, ids, w.T, w.H, w.W, out=kq_out, workspace=ws)
                 rf.rf_scatter_frames(kq_out, full_out, ids, w.T, w.N)
 
     times = {}
-    for dense in (False, True):
+    for mode in ("latent", "cache", "dense"):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         a.record()
-        run(dense)
+        run(mode)
         b.record()
         torch.cuda.synchronize()
-        times[dense] = a.elapsed_time(b)
-        print(f"[bench] schedule loop ({'dense' if dense else 'asynchronous'}): {times[dense]:.1f} ms",
-              file=sys.stderr, flush=True)
+        times[mode] = a.elapsed_time(b)
+        print(f"[bench] schedule loop ({mode}): {times[mode]:.1f} ms", file=sys.stderr, flush=True)
     led = accounting.schedule_attention_flops(plan, w.T, w.M, w.N, w.head_dim, w.heads)
-    del sets, lat, proj, kq_out, full_out
+    del sets, lat, proj, kq_out, full_out, store
     return {"T_steps": T_steps, "T_w": T_w, "T_mid": T_mid, "n_small": n_s, "n_large": n_l,
-            "steps": led["steps"], "async_ms": round(times[False], 2), "dense_ms": round(times[True], 2),
-            "speedup": round(times[True] / times[False], 4), "ideal_flop_ratio": round(led["ratio"], 4),
-            "tflops_async": round(led["flop"] / (times[False] * 1e-3) / 1e12, 1)}
+            "steps": led["steps"], "async_ms": round(times["latent"], 2),
+            "async_cache_ms": round(times["cache"], 2), "dense_ms": round(times["dense"], 2),
+            "speedup": round(times["dense"] / times["latent"], 4),
+            "speedup_cache": round(times["dense"] / times["cache"], 4),
+            "ideal_flop_ratio": round(led["ratio"], 4),
+            "tflops_async": round(led["flop"] / (times["latent"] * 1e-3) / 1e12, 1)}
 
 
 def rolling_cache(w, args):
