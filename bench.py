@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--no-cache", action="store_true")
     ap.add_argument("--no-schedule", action="store_true")
     ap.add_argument("--no-frame-mask", action="store_true")
+    ap.add_argument("--no-shard", action="store_true")
     ap.add_argument("--schedule", default="50,8,25,2,3",
                     help="T,T_w,T_mid,n_small,n_large of the multi-step schedule loop")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -265,6 +266,9 @@ def main():
     if not args.no_schedule:
         result["schedule"] = schedule_loop(w, ws, args)
 
+    if not args.no_shard:
+        result["head_shard"] = head_shard(w, args)
+
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
@@ -336,6 +340,38 @@ def frame_mask(w, q, k, v, ws, args):
     del out
     return {"kv_frames": list(w.keyframes), "avg_ms": round(ms, 4), "tflops": round(tf, 2),
             "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop}
+
+
+def head_shard(w, args):
+    """One GPU's share if the path were sharded by head over 8 GPUs: the same
+    frames and keyframes with heads / 8 heads (no exchange between GPUs is
+    needed, each holds its heads' full-length Q, K, V)."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    heads = max(1, w.heads // 8)
+    ws_ = workloads.custom(w.T, w.H, w.W, heads, w.head_dim, w.keyframes, dtype=w.dtype, seed=950)
+    q, k, v = workloads.make_qkv(ws_, device="cuda")
+    out = torch.empty((ws_.M * ws_.N, heads, ws_.head_dim), dtype=q.dtype, device="cuda")
+    wsp = torch.empty(max(16, rf.rf_attention_workspace(ws_.M, ws_.T, ws_.T, ws_.H, ws_.W, heads, ws_.head_dim,
+                                                        q.dtype)), dtype=torch.uint8, device="cuda")
+    rf.rf_keyframe_attention_ws(q, k, v, ws_.keyframes, ws_.T, ws_.H, ws_.W, out=out, workspace=wsp)
+    torch.cuda.synchronize()
+    n = max(3, args.steps)
+    ev = _events(n)
+    for a, b in ev:
+        a.record()
+        rf.rf_keyframe_attention_ws(q, k, v, ws_.keyframes, ws_.T, ws_.H, ws_.W, out=out, workspace=wsp)
+        b.record()
+    torch.cuda.synchronize()
+    ms = _avg_ms(ev)
+    flop = accounting.attention_flops(ws_.M * ws_.N, ws_.S, ws_.head_dim, heads)
+    tf = flop / (ms * 1e-3) / 1e12
+    print(f"[bench] one GPU's head share ({heads} of {w.heads} heads): {ms:.3f} ms = {tf:.1f} TFLOP/s",
+          file=sys.stderr, flush=True)
+    del q, k, v, out, wsp
+    return {"heads": heads, "of_heads": w.heads, "gpus": 8, "avg_ms": round(ms, 4), "tflops": round(tf, 2),
+            "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
 
 
 def schedule_loop(w, ws, args):
