@@ -32,6 +32,8 @@ def _case(B, C, T, H, W, dtype=torch.float32, seed=0, scale=1.0):
     (1, 2, 1, 9, 9),          # a single frame
     (1, 1, 256, 8, 8),        # the largest T (64-element chunks)
     (1, 2, 66, 40, 40),       # more block pairs than threads in a workgroup
+    (2, 2, 64, 12, 12),       # 16-byte staging path with the most frames it takes (64)
+    (1, 8, 33, 16, 20),       # 16-byte staging path, 33 frames (padded to 36)
 ])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_similarity_parity(shape, dtype):
