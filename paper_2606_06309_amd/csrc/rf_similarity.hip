@@ -10,7 +10,10 @@
 //     [element][frame], frames padded to a multiple of 4) and accumulates 4x4
 //     frame blocks of the Gram matrix in double precision (fp32 x fp32
 //     products are exact in double). The run's partial blocks go to the
-//     workspace.
+//     workspace. fp32 latents of at most 64 frames whose planes are a
+//     multiple of 4 take gram_partial_dma_kernel instead: the chunk's frame
+//     rows stream from HBM into LDS through the load units, double-buffered.
+//     About 512 workgroups in all (two per compute unit) cover the batch.
 //  2. gram_reduce_kernel: a workgroup per 4x4 block pair sums the partials of
 //     all runs in a fixed order (deterministic) into the output matrix.
 //  3. cosine_normalize_kernel: one workgroup per batch element turns G into
@@ -25,7 +28,7 @@ constexpr int kTileFloats = 16384;     // LDS floats for one staged chunk (64 KB
 constexpr int kMaxChunk = 256;         // feature elements per chunk
 constexpr double kNormFloor = 1e-8;
 #ifndef RF_SIM_TARGET_WORKGROUPS
-#define RF_SIM_TARGET_WORKGROUPS 1024
+#define RF_SIM_TARGET_WORKGROUPS 512
 #endif
 constexpr int64_t kTargetWorkgroups = RF_SIM_TARGET_WORKGROUPS;   // partial-Gram workgroups per launch
 constexpr int kNarrowFrames = 64;            // padded frame count of the register-sum path
@@ -178,6 +181,138 @@ __global__ __launch_bounds__(kThreads) void gram_partial_kernel(const PartialArg
     }
 }
 
+// 16 bytes per lane from a buffer resource straight into LDS (lane l lands at
+// dst + 16 l); offsets at or past the resource's range read as zero.
+__device__ __forceinline__ void sim_load_lds16(__amdgpu_buffer_rsrc_t r, __attribute__((address_space(3))) void *dst,
+                                               int voffset) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voffset, 0, 0, 0);
+}
+
+constexpr int kBufferWord3 = 0x00020000;   // raw buffer resource, gfx9-class GPUs
+
+// A pointer every lane holds the same value of, rebuilt from its first lane.
+__device__ __forceinline__ void *sim_uniform_ptr(const void *p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<void *>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Narrow path for fp32 latents whose planes are a multiple of 4 elements: a
+// chunk's frame rows (256 elements = 1 KB each, [frame][element] order) go
+// from HBM straight into LDS, one wave-wide 16-byte-per-lane load per row,
+// double-buffered so the next chunk streams in while this one is summed;
+// elements past the plane read as zero through the load's range check, the
+// padding frames' rows are zeroed once. A thread accumulates its 4x4 block pair
+// over groups of 4 consecutive elements (8 LDS reads of 16 bytes per 64 fused
+// multiply-adds).
+__global__ __launch_bounds__(kThreads) void gram_partial_dma_kernel(const PartialArgs a) {
+    constexpr int kL = kThreads;
+    constexpr int kGroups = kL / 4;
+    extern __shared__ __attribute__((aligned(1024))) float tile[];   // 2 x [Tp][kL] floats
+    const int64_t b = blockIdx.x / a.n_runs;
+    const int64_t rn = blockIdx.x - b * a.n_runs;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n_items = a.KS > 1 ? a.NBP * a.KS : a.NBP;
+    double *dst = a.ws + (b * a.n_runs + rn) * a.NBP * 16;
+    const int buf_floats = a.Tp * kL;
+
+    // padding frames: zero rows in both buffers (never loaded)
+    for (int i = tid; i < 2 * (a.Tp - a.T) * kL; i += kThreads) {
+        const int bufi = i / ((a.Tp - a.T) * kL);
+        const int rem = i - bufi * (a.Tp - a.T) * kL;
+        tile[bufi * buf_floats + a.T * kL + rem] = 0.0f;
+    }
+
+    const int64_t c0 = rn * a.run;
+    const int64_t c1 = (c0 + a.run < a.n_chunks) ? c0 + a.run : a.n_chunks;
+    // loads of chunk `chunk` into buffer `bufi`: wave w takes frames w, w + 4, ...
+    auto issue = [&](int64_t chunk, int bufi) {
+        const int64_t c = chunk / a.chunks_per_plane;
+        const int64_t p0 = (chunk - c * a.chunks_per_plane) * kL;
+        const float *base = static_cast<const float *>(a.x) + ((b * a.C + c) * a.T) * a.plane + p0;
+        const int64_t left = (static_cast<int64_t>(a.T) * a.plane - p0) * 4;
+        const int32_t rec = __builtin_amdgcn_readfirstlane(
+            static_cast<int32_t>(left < 0x7fffffffLL ? left : 0x7fffffffLL));
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(sim_uniform_ptr(base), 0, rec,
+                                                                            kBufferWord3);
+        const bool in = p0 + 4 * lane < a.plane;
+        for (int f = wave; f < a.T; f += kThreads / 64) {
+            const int off = in ? static_cast<int>(f * a.plane * 4 + lane * 16) : static_cast<int>(0xfffffff0u);
+            sim_load_lds16(r, (__attribute__((address_space(3))) void *)(
+                                  reinterpret_cast<char *>(tile) + (bufi * buf_floats + f * kL) * 4),
+                           off);
+        }
+    };
+    auto done = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this wave's loads have reached LDS
+        __syncthreads();
+    };
+
+    double acc[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0;
+    int bi = 0, bj = 0, ks = 0;
+    if (tid < n_items) {
+        const int bp = a.KS > 1 ? tid / a.KS : tid;
+        ks = a.KS > 1 ? tid - bp * a.KS : 0;
+        block_pair(bp, a.NB, bi, bj);
+    }
+    auto sum_chunk = [&](int bufi) {
+        if (tid >= n_items) return;
+        const f32x4_t *t4 = reinterpret_cast<const f32x4_t *>(tile + bufi * buf_floats);
+        for (int g = ks; g < kGroups; g += a.KS) {
+            f32x4_t u[4], w[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                u[r] = t4[(4 * bi + r) * kGroups + g];
+                w[r] = t4[(4 * bj + r) * kGroups + g];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        acc[r * 4 + q] = fma(static_cast<double>(u[r][e]), static_cast<double>(w[q][e]),
+                                             acc[r * 4 + q]);
+        }
+    };
+    if (c0 < c1) issue(c0, 0);
+    done();
+    for (int64_t chunk = c0; chunk < c1; chunk += 2) {
+        if (chunk + 1 < c1) issue(chunk + 1, 1);
+        sum_chunk(0);
+        done();
+        if (chunk + 1 >= c1) break;
+        if (chunk + 2 < c1) issue(chunk + 2, 0);
+        sum_chunk(1);
+        done();
+    }
+    if (a.KS == 1) {
+        if (tid < n_items) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) dst[tid * 16 + e] = acc[e];
+        }
+    } else {
+        double *red = reinterpret_cast<double *>(tile);
+        __syncthreads();
+        if (tid < n_items) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) red[tid * 16 + e] = acc[e];
+        }
+        __syncthreads();
+        for (int t = tid; t < a.NBP * 16; t += kThreads) {
+            const int bq = t / 16, e = t - bq * 16;
+            double sum = 0.0;
+            for (int j = 0; j < a.KS; ++j) sum += red[(bq * a.KS + j) * 16 + e];
+            dst[t] = sum;
+        }
+    }
+}
+
 struct ReduceArgs {
     const double *ws;
     double *sim;
@@ -276,7 +411,21 @@ hipError_t launch_similarity(const SimParams &p, hipStream_t stream) {
     size_t lds = static_cast<size_t>(g.Tp) * g.L * sizeof(float);
     const size_t red = static_cast<size_t>(kThreads) * 16 * sizeof(double);
     if (!wide && a.KS > 1 && lds < red) lds = red;
-    if (p.dtype == RF_BF16) {
+    // fp32, at most 64 frames, planes of a multiple of 4 elements and frame blocks
+    // addressable with 32-bit offsets: chunks streamed into LDS by the load units
+    const bool dma = p.dtype == RF_F32 && !wide && p.plane % 4 == 0 &&
+                     static_cast<int64_t>(p.T) * p.plane * 4 < 0x7ffff000LL;
+    if (dma) {
+        const size_t two = 2 * static_cast<size_t>(g.Tp) * g.L * sizeof(float);
+        const size_t bytes = two > lds ? two : lds;
+        if (bytes > 65536) {   // more than 64 KB of dynamic LDS must be allowed explicitly
+            const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&gram_partial_dma_kernel),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     static_cast<int>(bytes));
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(gram_partial_dma_kernel, grid, block, bytes, stream, a);
+    } else if (p.dtype == RF_BF16) {
         if (wide) hipLaunchKernelGGL((gram_partial_kernel<true, true>), grid, block, lds, stream, a);
         else hipLaunchKernelGGL((gram_partial_kernel<true, false>), grid, block, lds, stream, a);
     } else {
