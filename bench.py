@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--no-schedule", action="store_true")
     ap.add_argument("--no-frame-mask", action="store_true")
     ap.add_argument("--no-shard", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--schedule", default="50,8,25,2,3",
                     help="T,T_w,T_mid,n_small,n_large of the multi-step schedule loop")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -269,6 +270,9 @@ def main():
     if not args.no_shard:
         result["head_shard"] = head_shard(w, args)
 
+    if not args.no_peaks:
+        result["measured_peaks"] = measured_peaks(attn_tflops)
+
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
@@ -340,6 +344,80 @@ def frame_mask(w, q, k, v, ws, args):
     del out
     return {"kv_frames": list(w.keyframes), "avg_ms": round(ms, 4), "tflops": round(tf, 2),
             "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop}
+
+
+def measured_peaks(attn_tflops):
+    """What this device sustains under a pure load of one kind, beside the
+    published peaks: the dense bf16 matrix cores (probe kernel of independent
+    32x32x16 MFMA chains over random normal operands that change from one
+    instruction to the next, 4 workgroups of 4 waves per compute unit, launches
+    back to back, the second half averaged; the clock it implies at 4096 FLOP
+    per CU and cycle; the same on zero operands, which do not toggle), the
+    vendor library's 8192^3 bf16 product as a reference point, and HBM reads
+    (2 GiB, far beyond the 256 MB Infinity Cache, best of three grid sizes)."""
+    import torch
+    from paper_2606_06309_amd import binding as rf
+
+    wg, rounds, n = 1024, 5000, 10
+
+    def probe(ops):
+        sink = rf.rf_probe_mfma_bf16(ops, wg, 2)
+        torch.cuda.synchronize()
+        ev = _events(n)
+        for a, b in ev:
+            a.record()
+            rf.rf_probe_mfma_bf16(ops, wg, rounds, sink=sink)
+            b.record()
+        torch.cuda.synchronize()
+        return wg * rounds * 2.0 ** 22 / (_avg_ms(ev[n // 2:]) * 1e-3) / 1e12
+
+    g = torch.Generator(device="cpu").manual_seed(7)
+    mfma_tf = probe(torch.randn((16, 64, 8), generator=g).to(torch.bfloat16).cuda())
+    mfma_zero_tf = probe(torch.zeros((16, 64, 8), dtype=torch.bfloat16, device="cuda"))
+    clock = mfma_tf * 1e12 / (256 * 4096) / 1e9
+
+    # the vendor library's large product on the same kind of data (a reference point only)
+    ga = torch.randn((8192, 8192), generator=g).to(torch.bfloat16).cuda()
+    gb = torch.randn((8192, 8192), generator=g).to(torch.bfloat16).cuda()
+    gc = torch.matmul(ga, gb)
+    torch.cuda.synchronize()
+    ev = _events(n)
+    for a, b in ev:
+        a.record()
+        torch.matmul(ga, gb, out=gc)
+        b.record()
+    torch.cuda.synchronize()
+    gemm_tf = 2.0 * 8192 ** 3 / (_avg_ms(ev[n // 2:]) * 1e-3) / 1e12
+    del ga, gb, gc
+
+    nbytes = 2 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    best = (0.0, 0)
+    for wgr in (1024, 2048, 4096):
+        sink = rf.rf_probe_hbm_read(src, wgr)
+        torch.cuda.synchronize()
+        ev = _events(5)
+        for a, b in ev:
+            a.record()
+            rf.rf_probe_hbm_read(src, wgr, sink=sink)
+            b.record()
+        torch.cuda.synchronize()
+        gbs = nbytes / (_avg_ms(ev) * 1e-3) / 1e9
+        best = max(best, (gbs, wgr))
+        del sink
+    del src
+    print(f"[bench] measured peaks: bf16 MFMA {mfma_tf:.0f} TFLOP/s on random operands (clock {clock:.2f} GHz), "
+          f"{mfma_zero_tf:.0f} on zero operands; library GEMM {gemm_tf:.0f}; HBM read {best[0]:.0f} GB/s",
+          file=sys.stderr, flush=True)
+    return {"mfma_bf16": {"tflops": round(mfma_tf, 1), "spec_tflops": PEAK_BF16_TFLOPS,
+                          "frac_spec": round(mfma_tf / PEAK_BF16_TFLOPS, 4), "clock_ghz": round(clock, 3),
+                          "workgroups": wg, "rounds": rounds, "operands": "random normal bf16",
+                          "launches_averaged": n - n // 2, "zero_operands_tflops": round(mfma_zero_tf, 1)},
+            "library_gemm_bf16": {"tflops": round(gemm_tf, 1), "shape": [8192, 8192, 8192],
+                                  "call": "torch.matmul, random normal bf16"},
+            "hbm_read": {"gbs": round(best[0], 1), "spec_gbs": PEAK_HBM_GBS,
+                         "frac_spec": round(best[0] / PEAK_HBM_GBS, 4), "bytes": nbytes, "workgroups": best[1]},
+            "attention_frac_of_measured_mfma": round(attn_tflops / mfma_tf, 4)}
 
 
 def head_shard(w, args):

@@ -12,7 +12,9 @@
  * them, the content-aware keyframe selection of Sec. 3.1 (frame similarity and
  * Alg. 1's scan), the per-layer rolling cache of App. B.2, whose projected
  * hidden states are the skipped frames' keys and values, and the progressive
- * asynchronous schedule (Eq. 2, Alg. 2) that says which step is which.
+ * asynchronous schedule (Eq. 2, Alg. 2) that says which step is which. Two
+ * device probes, measurement support outside the method, report the rates the
+ * matrix cores and HBM sustain on this device.
  *
  * Conventions shared by every call:
  *  - Return value: RF_OK (0) or a negative rf_status. No C++ exception crosses
@@ -31,7 +33,7 @@
  *    synchronisation, not as a return code.
  *  - Calls hold no global state and may be made from several threads.
  *  - Device pointers must be 16-byte aligned (128-bit accesses), otherwise
- *    RF_ERR_UNSUPPORTED.
+ *    RF_ERR_UNSUPPORTED, unless a call states a weaker requirement.
  */
 #ifndef RHYMEFLOW_H
 #define RHYMEFLOW_H
@@ -458,6 +460,48 @@ typedef struct rf_step_plan {
  */
 int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, int32_t n_large,
                       rf_step_plan *plan_out, int32_t *n_rhythmic_out, int32_t *n_skipped_out);
+
+/* ---- Device probes (measurement support, not part of the method) ----
+ * Sustained whole-chip rates of this device under a pure load of one kind, to
+ * set a kernel's achieved rate against what the device delivers besides the
+ * published peaks (MI355X: dense bf16 matrix 2.5 PFLOP/s at 2.4 GHz, HBM3E
+ * 8 TB/s); the chip runs below that clock when all matrix cores are busy.
+ * Both enqueue one kernel on `stream` and return at once; time them with
+ * events on that stream. Workgroups have 256 threads.
+ */
+
+/*
+ * Dense bf16 matrix cores: each of the workgroups' 4 waves runs 4 independent
+ * accumulator chains of 32x32x16 bf16 matrix multiply-accumulates (fp32
+ * accumulators), `rounds` rounds of 8 steps each. FLOP per launch:
+ * workgroups * rounds * 2^22.
+ * operands: device bf16 [16][64][8], 16-byte aligned: lane l holds A operands
+ * i = 0..7 (operands[i][l][0..7]) and B operands (operands[8 + i][l][0..7]);
+ * step u of chain j adds A[(u + 2j) % 8] B[(3u + j) % 8], where an A operand
+ * is the 32x16 matrix whose element (m, k) lane m + 32 (k / 8) holds at k % 8,
+ * a B operand the 16x32 matrix whose element (k, n) lane n + 32 (k / 8) holds
+ * at k % 8. Random operands make the matrix cores draw the power of a real
+ * product; small integers make the result exact.
+ * sink: device float [workgroups * 256], 4-byte aligned; thread i of a wave
+ * (lane l) writes the sum of its 64 accumulators, accumulator r of chain j
+ * being element (8 (r / 4) + 4 (l / 32) + r % 4, l % 32) of chain j's product.
+ * workgroups 1..2^20 (4 per compute unit give MI355X's 256 CUs 4 waves per
+ * SIMD), rounds 1..2^22. Errors: RF_ERR_INVALID_ARG (NULL), RF_ERR_RANGE
+ * (workgroups, rounds), RF_ERR_UNSUPPORTED (alignment).
+ */
+int rf_probe_mfma_bf16(const void *operands, int32_t workgroups, int32_t rounds, float *sink, void *stream);
+
+/*
+ * HBM reads: the workgroups read the device buffer src of `bytes` bytes once
+ * (16-byte words, grid-stride, streaming loads) and thread i writes the XOR of
+ * the 32-bit words it read to sink[i], so the XOR of sink[0 .. workgroups*256)
+ * is the XOR of every 32-bit word of src. Bytes per launch: `bytes`.
+ * src: 16-byte aligned, bytes a positive multiple of 16. sink: device
+ * uint32 [workgroups * 256], 4-byte aligned. workgroups 1..2^20.
+ * Errors: RF_ERR_INVALID_ARG (NULL, bytes), RF_ERR_RANGE (workgroups),
+ * RF_ERR_UNSUPPORTED (alignment).
+ */
+int rf_probe_hbm_read(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink, void *stream);
 
 #ifdef __cplusplus
 }

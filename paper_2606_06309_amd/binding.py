@@ -36,6 +36,7 @@ EXPORTED = [
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
     "rf_cache_project_kv", "rf_async_schedule",
+    "rf_probe_mfma_bf16", "rf_probe_hbm_read",
 ]
 
 RF_STEP_WARMUP = 0
@@ -146,6 +147,10 @@ lib.rf_cache_project_kv.argtypes = [_cachep, _vp, _vp, _vp, _i32p, _i32, ctypes.
 lib.rf_cache_project_kv.restype = ctypes.c_int
 lib.rf_async_schedule.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(rf_step_plan), _i32p, _i32p]
 lib.rf_async_schedule.restype = ctypes.c_int
+lib.rf_probe_mfma_bf16.argtypes = [_vp, _i32, _i32, _vp, _vp]
+lib.rf_probe_mfma_bf16.restype = ctypes.c_int
+lib.rf_probe_hbm_read.argtypes = [_vp, _i64, _i32, _vp, _vp]
+lib.rf_probe_hbm_read.restype = ctypes.c_int
 
 
 def _check(status: int):
@@ -494,3 +499,35 @@ def rf_async_schedule(T: int, T_w: int, T_mid: int, n_small: int, n_large: int):
                         t_start=p.t_start if skip else None, t_end=p.t_end if skip else None,
                         alpha=p.alpha if skip else None))
     return out
+
+
+# --- device probes (measurement support) ------------------------------------------
+
+PROBE_THREADS = 256
+
+
+def rf_probe_mfma_bf16(operands: torch.Tensor, workgroups: int, rounds: int, sink=None, stream=None):
+    """Enqueues the dense bf16 matrix-core probe (workgroups * rounds * 2^22
+    FLOP) on operands, bf16 [16][64][8]; returns the sink, float
+    [workgroups * 256] on the operands' device."""
+    if operands.dtype != torch.bfloat16 or operands.numel() != 16 * 64 * 8:
+        raise ValueError("operands must be bf16 with 16 * 64 * 8 elements")
+    if sink is None:
+        sink = torch.empty(workgroups * PROBE_THREADS, dtype=torch.float32, device=operands.device)
+    if sink.dtype != torch.float32 or sink.numel() < workgroups * PROBE_THREADS:
+        raise ValueError("sink must be float32 with workgroups * 256 elements")
+    _check(lib.rf_probe_mfma_bf16(_dev(operands, "operands"), workgroups, rounds, _dev(sink, "sink"),
+                                  _stream(stream)))
+    return sink
+
+
+def rf_probe_hbm_read(src: torch.Tensor, workgroups: int, sink=None, stream=None):
+    """Enqueues the HBM read probe over src's bytes; returns the sink, int32
+    [workgroups * 256] whose XOR is the XOR of src's 32-bit words."""
+    if sink is None:
+        sink = torch.empty(workgroups * PROBE_THREADS, dtype=torch.int32, device=src.device)
+    if sink.element_size() != 4 or sink.numel() < workgroups * PROBE_THREADS:
+        raise ValueError("sink must have 4-byte elements, workgroups * 256 of them")
+    _check(lib.rf_probe_hbm_read(_dev(src, "src"), src.numel() * src.element_size(), workgroups,
+                                 _dev(sink, "sink"), _stream(stream)))
+    return sink

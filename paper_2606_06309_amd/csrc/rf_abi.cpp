@@ -696,4 +696,29 @@ int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, in
     return ok();
 }
 
+int rf_probe_mfma_bf16(const void *operands, int32_t workgroups, int32_t rounds, float *sink, void *stream) {
+    const char *fn = "rf_probe_mfma_bf16";
+    if (!operands || !sink) return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);
+    if (workgroups < 1 || workgroups > (1 << 20) || rounds < 1 || rounds > (1 << 22))
+        return fail(RF_ERR_RANGE, "%s: workgroups %d (1..2^20) or rounds %d (1..2^22) out of range", fn,
+                    workgroups, rounds);
+    if (!aligned16(operands) || (reinterpret_cast<uintptr_t>(sink) & 3u))
+        return fail(RF_ERR_UNSUPPORTED, "%s: operands must be 16-byte and sink 4-byte aligned", fn);
+    return launched(rf::launch_mfma_probe(operands, workgroups, rounds, sink, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+int rf_probe_hbm_read(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink, void *stream) {
+    const char *fn = "rf_probe_hbm_read";
+    if (!src || !sink) return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);
+    if (bytes < 16 || bytes % 16 != 0)
+        return fail(RF_ERR_INVALID_ARG, "%s: bytes = %lld must be a positive multiple of 16", fn,
+                    static_cast<long long>(bytes));
+    if (workgroups < 1 || workgroups > (1 << 20))
+        return fail(RF_ERR_RANGE, "%s: workgroups %d out of range (1..2^20)", fn, workgroups);
+    if (!aligned16(src) || (reinterpret_cast<uintptr_t>(sink) & 3u))
+        return fail(RF_ERR_UNSUPPORTED, "%s: src must be 16-byte and sink 4-byte aligned", fn);
+    return launched(rf::launch_hbm_read_probe(src, bytes, workgroups, sink, static_cast<hipStream_t>(stream)), fn);
+}
+
 }  // extern "C"

@@ -120,4 +120,11 @@ struct SimParams {
 
 hipError_t launch_similarity(const SimParams &p, hipStream_t stream);
 
+// Device probes (measurement support): threads per workgroup of both probes.
+constexpr int kProbeThreads = 256;
+hipError_t launch_mfma_probe(const void *ops, int32_t workgroups, int32_t rounds, float *sink,
+                             hipStream_t stream);
+hipError_t launch_hbm_read_probe(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink,
+                                 hipStream_t stream);
+
 }  // namespace rf

@@ -249,3 +249,35 @@ def test_frame_copy_validation(fn, args, status):
     got = getattr(lib, fn)(a["src"], a["dst"], ids, len(a["ids"]), a["T"], a["rows"],
                            a["row_bytes"], None)
     assert got == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(ops=None), rf.RF_ERR_INVALID_ARG),
+    (dict(sink=None), rf.RF_ERR_INVALID_ARG),
+    (dict(wg=0), rf.RF_ERR_RANGE),
+    (dict(wg=(1 << 20) + 1), rf.RF_ERR_RANGE),
+    (dict(rounds=0), rf.RF_ERR_RANGE),
+    (dict(rounds=(1 << 22) + 1), rf.RF_ERR_RANGE),
+    (dict(ops=A + 8), rf.RF_ERR_UNSUPPORTED),
+    (dict(sink=B_ + 2), rf.RF_ERR_UNSUPPORTED),
+])
+def test_mfma_probe_validation(args, status):
+    a = dict(ops=A, wg=4, rounds=8, sink=B_)
+    a.update(args)
+    assert lib.rf_probe_mfma_bf16(a["ops"], a["wg"], a["rounds"], a["sink"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(src=None), rf.RF_ERR_INVALID_ARG),
+    (dict(sink=None), rf.RF_ERR_INVALID_ARG),
+    (dict(nbytes=0), rf.RF_ERR_INVALID_ARG),
+    (dict(nbytes=24), rf.RF_ERR_INVALID_ARG),
+    (dict(nbytes=-16), rf.RF_ERR_INVALID_ARG),
+    (dict(wg=0), rf.RF_ERR_RANGE),
+    (dict(src=A + 8), rf.RF_ERR_UNSUPPORTED),
+    (dict(sink=B_ + 1), rf.RF_ERR_UNSUPPORTED),
+])
+def test_hbm_probe_validation(args, status):
+    a = dict(src=A, nbytes=4096, wg=4, sink=B_)
+    a.update(args)
+    assert lib.rf_probe_hbm_read(a["src"], a["nbytes"], a["wg"], a["sink"], None) == status
