@@ -289,11 +289,22 @@ def test_split_tail_long_workload():
     assert_parity(got, ref, "bf16", "long split tail")
 
 
-def test_frame_attention_split_tail():
-    w = workloads.custom(12, 16, 16, 2, 128, (0, 4, 8), dtype="bf16", seed=55)
-    kvf = (0, 1, 2, 4, 5, 7, 8, 9, 10, 11)    # 40 key tiles
+FRAME_SPLIT_CASES = [
+    # frames of 256 keys (4 whole tiles each): 40 key tiles
+    (workloads.custom(12, 16, 16, 2, 128, (0, 4, 8), dtype="bf16", seed=55), (0, 1, 2, 4, 5, 7, 8, 9, 10, 11)),
+    # ragged frames of 130 keys (3 tiles, the last with 2 keys): 18 key tiles, parts start inside frames
+    (workloads.custom(9, 10, 13, 3, 128, (0, 4, 8), dtype="bf16", seed=56), (0, 1, 3, 4, 6, 8)),
+    (workloads.custom(9, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=57), (1, 2, 3, 4, 5, 7, 8)),
+]
+
+
+@pytest.mark.parametrize("case", FRAME_SPLIT_CASES,
+                         ids=lambda c: f"N{c[0].N}_d{c[0].head_dim}_kv{len(c[1])}")
+def test_frame_attention_split_tail(case):
+    w, kvf = case
     need = rf.rf_attention_workspace(w.M, len(kvf), w.T, w.H, w.W, w.heads, w.head_dim, w.torch_dtype)
-    assert need > 0
+    assert need > 0, "case must exercise the split"
+    print(f"[case] frame-mask split N={w.N} d={w.head_dim} kv={kvf}", flush=True)
     q, k, v = workloads.make_qkv(w, device="cuda")
     ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
     out = rf.rf_frame_attention(q, k, v, w.keyframes, kvf, w.T, w.H, w.W, workspace=ws)
