@@ -39,7 +39,8 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed steps first (the clock takes a few hundred ms to settle under load)")
     ap.add_argument("--workload", default="long",
                     help="long (default), 720p, 480p, small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
