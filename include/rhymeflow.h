@@ -127,8 +127,9 @@ int rf_keyframes_uniform(int32_t T, int32_t M, int32_t *ids_out, int32_t *n_out)
  * dtype:   RF_F32 or RF_BF16 storage for latents and out (fp32 arithmetic;
  *          bf16 results rounded to nearest even).
  * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0, non-finite timesteps, partial
- *         overlap of out and latents), RF_ERR_RANGE (T > RF_MAX_FRAMES),
- *         RF_ERR_UNSUPPORTED (unknown dtype, misaligned pointer), RF_ERR_HIP.
+ *         overlap of out and latents), RF_ERR_RANGE (T > RF_MAX_FRAMES, sizes
+ *         whose byte counts would pass 4e18), RF_ERR_UNSUPPORTED (unknown dtype,
+ *         misaligned pointer), RF_ERR_HIP.
  */
 int rf_project_latents(const void *latents, void *out, const double timesteps[3],
                        const uint8_t *keyframe_mask, int32_t B, int32_t C,
@@ -155,8 +156,8 @@ int rf_project_latents(const void *latents, void *out, const double timesteps[3]
  *          even) or RF_F32 (fp32 throughout, a correctness path).
  * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0, ids not strictly increasing,
  *         out overlapping an input), RF_ERR_RANGE (an id outside [0, T), M > T,
- *         T > RF_MAX_FRAMES), RF_ERR_UNSUPPORTED (head_dim, dtype, alignment),
- *         RF_ERR_HIP.
+ *         T > RF_MAX_FRAMES, sizes whose byte counts would pass 4e18),
+ *         RF_ERR_UNSUPPORTED (head_dim, dtype, alignment), RF_ERR_HIP.
  */
 int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out,
                           const int32_t *keyframe_ids, int32_t M, int32_t T,
@@ -189,7 +190,8 @@ int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *
  * Bytes of workspace rf_keyframe_attention_ws (Mkv = T) or rf_frame_attention
  * (Mkv key/value frames) uses for these sizes (host only; 0 when nothing is
  * split, always 0 for RF_F32). The split assumes MI355X's 256 compute units.
- * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (T, M, Mkv),
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (T, M, Mkv, sizes
+ *         whose byte counts would pass 4e18),
  * RF_ERR_UNSUPPORTED (head_dim, dtype).
  */
 int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
@@ -230,7 +232,8 @@ int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
  * src_full: device, T*N rows. dst_compact: device, M*N rows; no overlap.
  * frame_ids: host [M], strictly increasing, each in [0, T).
  * row_bytes: a multiple of 16.
- * Errors: RF_ERR_INVALID_ARG, RF_ERR_RANGE, RF_ERR_UNSUPPORTED (alignment,
+ * Errors: RF_ERR_INVALID_ARG, RF_ERR_RANGE (ids, T, rows_per_frame * row_bytes *
+ *         RF_MAX_FRAMES past 4e18), RF_ERR_UNSUPPORTED (alignment,
  *         row_bytes % 16), RF_ERR_HIP.
  */
 int rf_gather_frames(const void *src_full, void *dst_compact,

@@ -26,6 +26,10 @@ int ok() {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Byte counts are 64-bit: sizes whose product (computed in double) passes this
+// are rejected before any of it is formed in integers.
+constexpr double kMaxBytes = 4.0e18;
+
 // Half-open byte ranges [a, a+na) and [b, b+nb) intersect.
 bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
     const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
@@ -150,6 +154,8 @@ int rf_project_latents(const void *latents, void *out, const double timesteps[3]
     if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
     if (dtype != RF_F32 && dtype != RF_BF16)
         return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (static_cast<double>(B) * 2.0 * C * T * Hl * Wl * 4.0 > kMaxBytes)
+        return fail(RF_ERR_RANGE, "%s: sizes overflow 64-bit byte counts", fn);
     const double t_start = timesteps[0], t_end = timesteps[1], tau = timesteps[2];
     if (!isfinite(t_start) || !isfinite(t_end) || !isfinite(tau))
         return fail(RF_ERR_INVALID_ARG, "%s: timesteps must be finite", fn);
@@ -207,6 +213,9 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
     if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
                     fn, H, W, heads, head_dim);
+    if (static_cast<double>(H) * W * (T > 0 ? T : 1) * heads * head_dim * 4.0 > kMaxBytes)
+        return fail(RF_ERR_RANGE, "%s: sizes overflow 64-bit byte counts (T=%d H=%d W=%d heads=%d head_dim=%d)",
+                    fn, T, H, W, heads, head_dim);
     rf::AttnParams p{};
     int rc = check_id_list(q_ids, M, T, p.kf, fn);
     if (rc != RF_OK) return rc;
@@ -299,6 +308,8 @@ int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t
     if (head_dim != 64 && head_dim != 128)
         return fail(RF_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
     if (dtype != RF_BF16 && dtype != RF_F32) return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
+    if (static_cast<double>(H) * W * T * heads * head_dim * 4.0 > kMaxBytes)
+        return fail(RF_ERR_RANGE, "%s: sizes overflow 64-bit byte counts", fn);
     *bytes_out = attention_ws_need(M, Mkv < T ? Mkv : 0, T, static_cast<int64_t>(H) * W, heads, head_dim, dtype);
     return ok();
 }
@@ -309,6 +320,8 @@ static int frame_copy(const void *src, void *dst, const int32_t *frame_ids, int3
     if (!src || !dst) return fail(RF_ERR_INVALID_ARG, "%s: NULL buffer", fn);
     if (rows_per_frame <= 0 || row_bytes <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: rows_per_frame and row_bytes must be positive", fn);
+    if (static_cast<double>(rows_per_frame) * static_cast<double>(row_bytes) * RF_MAX_FRAMES > kMaxBytes)
+        return fail(RF_ERR_RANGE, "%s: rows_per_frame x row_bytes overflows 64-bit byte counts", fn);
     rf::FrameCopyParams p{};
     int32_t ids[RF_MAX_FRAMES];
     const int rc = check_id_list(frame_ids, M, T, ids, fn);
@@ -354,8 +367,8 @@ int rf_frame_similarity_workspace(int32_t B, int32_t C, int32_t T, int32_t H, in
                     fn, B, C, T, H, W);
     if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
     const rf::SimGeometry g = rf::similarity_geometry(B, C, T, static_cast<int64_t>(H) * W);
-    if (static_cast<double>(B) * static_cast<double>(g.n_runs) * g.NBP * 128.0 > 4.0e18 ||
-        static_cast<double>(C) * H * W * T * B > 4.0e18)
+    if (static_cast<double>(B) * static_cast<double>(g.n_runs) * g.NBP * 128.0 > kMaxBytes ||
+        static_cast<double>(C) * H * W * T * B > kMaxBytes)
         return fail(RF_ERR_RANGE, "%s: workspace size overflows", fn);
     *bytes_out = g.workspace_bytes;
     return ok();
@@ -447,7 +460,7 @@ static int cache_store_bytes(int32_t n_cached, int64_t rows_per_frame, int32_t h
     if (n_cached > RF_MAX_FRAMES)
         return fail(RF_ERR_RANGE, "%s: n_cached = %d exceeds %d", fn, n_cached, RF_MAX_FRAMES);
     if (dtype != RF_F32 && dtype != RF_BF16) return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
-    if (static_cast<double>(rows_per_frame) * hidden * elem_bytes(dtype) * 2.0 * n_cached * RF_MAX_FRAMES > 4.0e18)
+    if (static_cast<double>(rows_per_frame) * hidden * elem_bytes(dtype) * 2.0 * n_cached * RF_MAX_FRAMES > kMaxBytes)
         return fail(RF_ERR_RANGE, "%s: size overflows", fn);
     *bytes_out = 2 * static_cast<int64_t>(n_cached) * rows_per_frame * hidden * elem_bytes(dtype);
     return RF_OK;

@@ -281,3 +281,19 @@ def test_hbm_probe_validation(args, status):
     a = dict(src=A, nbytes=4096, wg=4, sink=B_)
     a.update(args)
     assert lib.rf_probe_hbm_read(a["src"], a["nbytes"], a["wg"], a["sink"], None) == status
+
+
+def test_sizes_overflowing_byte_counts_are_range_errors():
+    """Sizes whose byte counts would pass 64 bits are rejected before any is
+    formed in integers (and before any HIP call)."""
+    big = 2 ** 31 - 1
+    ids = (ctypes.c_int32 * 2)(0, 1)
+    assert lib.rf_keyframe_attention(A, B_, A + 4096, B_ + 4096, ids, 2, 4, big, big, 8, 128,
+                                     rf.RF_BF16, None) == rf.RF_ERR_RANGE
+    n = ctypes.c_int64(0)
+    assert lib.rf_attention_workspace(2, 4, 4, big, big, 8, 128, rf.RF_BF16, ctypes.byref(n)) == rf.RF_ERR_RANGE
+    m = (ctypes.c_uint8 * 5)(1, 0, 1, 0, 1)
+    ts = (ctypes.c_double * 3)(24.0, 21.0, 23.0)
+    assert lib.rf_project_latents(A, B_, ts, m, big, 16, 5, big, 16, rf.RF_F32, None) == rf.RF_ERR_RANGE
+    for fn in (lib.rf_gather_frames, lib.rf_scatter_frames):
+        assert fn(A, B_, ids, 2, 4, 2 ** 40, 2 ** 32, None) == rf.RF_ERR_RANGE
