@@ -480,6 +480,7 @@ static int check_cache(const rf_rolling_cache *c, const char *fn) {
     if (c->magic != kCacheMagic) return fail(RF_ERR_INVALID_ARG, "%s: cache not initialised by rf_cache_init", fn);
     if (c->T <= 0 || c->T > RF_MAX_FRAMES || c->n_cached <= 0 || c->n_cached > c->T ||
         c->rows_per_frame <= 0 || c->hidden <= 0 || (c->dtype != RF_F32 && c->dtype != RF_BF16) ||
+        static_cast<double>(c->rows_per_frame) * c->hidden * 4.0 * 2.0 * RF_MAX_FRAMES > kMaxBytes ||
         c->frame_bytes != c->rows_per_frame * c->hidden * elem_bytes(c->dtype))
         return fail(RF_ERR_INVALID_ARG, "%s: cache struct is inconsistent", fn);
     for (int32_t f = 0; f < c->T; ++f) {
