@@ -373,8 +373,8 @@ def measured_peaks(attn_tflops):
         return wg * rounds * 2.0 ** 22 / (_avg_ms(ev[n // 2:]) * 1e-3) / 1e12
 
     g = torch.Generator(device="cpu").manual_seed(7)
-    mfma_tf = probe(torch.randn((16, 64, 8), generator=g).to(torch.bfloat16).cuda())
-    mfma_zero_tf = probe(torch.zeros((16, 64, 8), dtype=torch.bfloat16, device="cuda"))
+    mfma_tf = probe(torch.randn((12, 64, 8), generator=g).to(torch.bfloat16).cuda())
+    mfma_zero_tf = probe(torch.zeros((12, 64, 8), dtype=torch.bfloat16, device="cuda"))
     clock = mfma_tf * 1e12 / (256 * 4096) / 1e9
 
     # the vendor library's large product on the same kind of data (a reference point only)

@@ -478,13 +478,14 @@ int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, in
  * accumulator chains of 32x32x16 bf16 matrix multiply-accumulates (fp32
  * accumulators), `rounds` rounds of 8 steps each. FLOP per launch:
  * workgroups * rounds * 2^22.
- * operands: device bf16 [16][64][8], 16-byte aligned: lane l holds A operands
- * i = 0..7 (operands[i][l][0..7]) and B operands (operands[8 + i][l][0..7]);
- * step u of chain j adds A[(u + 2j) % 8] B[(3u + j) % 8], where an A operand
- * is the 32x16 matrix whose element (m, k) lane m + 32 (k / 8) holds at k % 8,
- * a B operand the 16x32 matrix whose element (k, n) lane n + 32 (k / 8) holds
- * at k % 8. Random operands make the matrix cores draw the power of a real
- * product; small integers make the result exact.
+ * operands: device bf16 [12][64][8], 16-byte aligned: lane l holds A operands
+ * i = 0..5 (operands[i][l][0..7]) and B operands (operands[6 + i][l][0..7]);
+ * step u (0..7) of chain j adds A[(u + 2j) % 6] B[(3u + j) % 6], where an A
+ * operand is the 32x16 matrix whose element (m, k) lane m + 32 (k / 8) holds
+ * at k % 8, a B operand the 16x32 matrix whose element (k, n) lane
+ * n + 32 (k / 8) holds at k % 8. Random operands make the matrix cores draw
+ * the power of a real product; small integers make the result exact. The
+ * kernel fits four waves on every SIMD.
  * sink: device float [workgroups * 256], 4-byte aligned; thread i of a wave
  * (lane l) writes the sum of its 64 accumulators, accumulator r of chain j
  * being element (8 (r / 4) + 4 (l / 32) + r % 4, l % 32) of chain j's product.

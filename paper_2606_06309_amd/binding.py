@@ -508,10 +508,10 @@ PROBE_THREADS = 256
 
 def rf_probe_mfma_bf16(operands: torch.Tensor, workgroups: int, rounds: int, sink=None, stream=None):
     """Enqueues the dense bf16 matrix-core probe (workgroups * rounds * 2^22
-    FLOP) on operands, bf16 [16][64][8]; returns the sink, float
+    FLOP) on operands, bf16 [12][64][8]; returns the sink, float
     [workgroups * 256] on the operands' device."""
-    if operands.dtype != torch.bfloat16 or operands.numel() != 16 * 64 * 8:
-        raise ValueError("operands must be bf16 with 16 * 64 * 8 elements")
+    if operands.dtype != torch.bfloat16 or operands.numel() != 12 * 64 * 8:
+        raise ValueError("operands must be bf16 with 12 * 64 * 8 elements")
     if sink is None:
         sink = torch.empty(workgroups * PROBE_THREADS, dtype=torch.float32, device=operands.device)
     if sink.dtype != torch.float32 or sink.numel() < workgroups * PROBE_THREADS:

@@ -7,12 +7,17 @@
 //
 //  * mfma_probe_kernel: every wave runs kChains independent accumulator chains
 //    of v_mfma_f32_32x32x16_bf16 (independent chains keep the matrix core fed
-//    without waiting for a result). A lane holds 8 A and 8 B operands read
-//    once from the caller's buffer, and step u of a round multiplies A[(u + 2j)
-//    % 8] by B[(3u + j) % 8] in chain j, so consecutive instructions see
-//    different data, as in a real product (the power a matrix core draws, and
-//    with it the clock the chip holds, depends on how much its inputs change).
-//    A round is 8 steps of every chain: 2^22 FLOP per (workgroup, round).
+//    without waiting for a result). A lane holds 6 A and 6 B operands, and step
+//    u of a round multiplies A[(u + 2j) % 6] by B[(3u + j) % 6] in chain j, so
+//    consecutive instructions see different data, as in a real product (the
+//    power a matrix core draws, and with it the clock the chip holds, depends
+//    on how much its inputs change). A round is 8 steps of every chain: 2^22
+//    FLOP per (workgroup, round). The operands go from the caller's buffer into
+//    LDS and from there into registers, the path real kernels feed the matrix
+//    cores by: loaded straight from global memory into the operand registers,
+//    the same loop sustained well under the rate the hardware reaches. The
+//    kernel is held to four waves per SIMD (114 registers) so that a grid of 4
+//    workgroups per CU runs in one round.
 //  * hbm_read_kernel: a grid-stride read of 16-byte words (four loads in
 //    flight per thread), folded with XOR into one 32-bit word per thread, so
 //    the XOR of all sink words equals the XOR of all words of the buffer.
@@ -26,23 +31,27 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kChains = 4;
-constexpr int kOps = 8;   // A and B operands per lane
+constexpr int kOps = 6;   // A and B operands per lane
+constexpr int kSteps = 8; // steps of every chain per round
 
-__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(const u32x4_t *ops, int32_t rounds,
-                                                                   float *sink) {
+__global__ __launch_bounds__(kProbeThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void mfma_probe_kernel(const u32x4_t *ops, int32_t rounds, float *sink) {
+    __shared__ __attribute__((aligned(16))) u32x4_t staged[2 * kOps * 64];
+    for (int t = threadIdx.x; t < 2 * kOps * 64; t += kProbeThreads) staged[t] = ops[t];
+    __syncthreads();
     const int lane = threadIdx.x & 63;
     u32x4_t A[kOps], B[kOps];
 #pragma unroll
     for (int i = 0; i < kOps; ++i) {
-        A[i] = ops[i * 64 + lane];
-        B[i] = ops[(kOps + i) * 64 + lane];
+        A[i] = staged[i * 64 + lane];
+        B[i] = staged[(kOps + i) * 64 + lane];
     }
     f32x16_t c[kChains];
 #pragma unroll
     for (int j = 0; j < kChains; ++j) c[j] = f32x16_t{};
     for (int32_t it = 0; it < rounds; ++it) {
 #pragma unroll
-        for (int u = 0; u < kOps; ++u)
+        for (int u = 0; u < kSteps; ++u)
 #pragma unroll
             for (int j = 0; j < kChains; ++j) {
                 const bf16x8_t a = __builtin_bit_cast(bf16x8_t, A[(u + 2 * j) % kOps]);

@@ -17,15 +17,15 @@ rf = pytest.importorskip("paper_2606_06309_amd.binding")
 
 
 def _lane_sums(ops, rounds):
-    """ops: float array [16][64][8]; the probe's per-lane sink value."""
-    A = np.zeros((8, 32, 16))
-    B = np.zeros((8, 16, 32))
+    """ops: float array [12][64][8]; the probe's per-lane sink value."""
+    A = np.zeros((6, 32, 16))
+    B = np.zeros((6, 16, 32))
     for k in range(16):
-        A[:, :, k] = ops[:8, 32 * (k // 8):32 * (k // 8) + 32, k % 8]
-        B[:, k, :] = ops[8:, 32 * (k // 8):32 * (k // 8) + 32, k % 8]
+        A[:, :, k] = ops[:6, 32 * (k // 8):32 * (k // 8) + 32, k % 8]
+        B[:, k, :] = ops[6:, 32 * (k // 8):32 * (k // 8) + 32, k % 8]
     sums = np.zeros(64)
     for j in range(4):
-        C = rounds * sum(A[(u + 2 * j) % 8] @ B[(3 * u + j) % 8] for u in range(8))
+        C = rounds * sum(A[(u + 2 * j) % 6] @ B[(3 * u + j) % 6] for u in range(8))
         for lane in range(64):
             for r in range(16):
                 sums[lane] += C[8 * (r // 4) + 4 * (lane // 32) + r % 4, lane % 32]
@@ -36,7 +36,7 @@ def _lane_sums(ops, rounds):
 def test_mfma_probe_integer_operands(wg, rounds, seed):
     print(f"[case] mfma probe wg={wg} rounds={rounds} seed={seed}", flush=True)
     g = torch.Generator(device="cpu").manual_seed(seed)
-    ops = torch.randint(-3, 4, (16, 64, 8), generator=g).to(torch.bfloat16)
+    ops = torch.randint(-3, 4, (12, 64, 8), generator=g).to(torch.bfloat16)
     sink = rf.rf_probe_mfma_bf16(ops.cuda(), wg, rounds)
     torch.cuda.synchronize()
     want = np.tile(_lane_sums(ops.float().numpy().astype(np.float64), rounds), wg * 4)
@@ -46,7 +46,7 @@ def test_mfma_probe_integer_operands(wg, rounds, seed):
 
 
 def test_mfma_probe_all_ones():
-    ops = torch.ones((16, 64, 8), dtype=torch.bfloat16, device="cuda")
+    ops = torch.ones((12, 64, 8), dtype=torch.bfloat16, device="cuda")
     sink = rf.rf_probe_mfma_bf16(ops, 4, 100)
     torch.cuda.synchronize()
     assert bool((sink == 8192.0 * 100).all())
@@ -56,7 +56,7 @@ def test_mfma_probe_random_operands_close():
     """Random normal operands (the benchmark's): the sink matches the numpy
     sum to fp32 accumulation accuracy."""
     g = torch.Generator(device="cpu").manual_seed(7)
-    ops = torch.randn((16, 64, 8), generator=g).to(torch.bfloat16)
+    ops = torch.randn((12, 64, 8), generator=g).to(torch.bfloat16)
     sink = rf.rf_probe_mfma_bf16(ops.cuda(), 2, 3)
     torch.cuda.synchronize()
     want = np.tile(_lane_sums(ops.float().numpy().astype(np.float64), 3), 8)
