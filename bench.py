@@ -59,6 +59,17 @@ def parse():
     return ap.parse_args()
 
 
+def _side(name, fn, *args):
+    """Runs a side measurement; an exception in it is reported (stderr and the
+    JSON line) instead of costing the line itself. The timed step is not run
+    through this."""
+    try:
+        return fn(*args)
+    except Exception as e:   # noqa: BLE001 - any failure of a side section is reported, not raised
+        print(f"[bench] {name} failed: {e!r}", file=sys.stderr, flush=True)
+        return {"error": repr(e)[:300]}
+
+
 def _events(n):
     import torch
     return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -254,29 +265,29 @@ def main():
               f"(ideal {w.T / w.M:.3f})", file=sys.stderr, flush=True)
 
     if not args.no_bandwidth:
-        result["bandwidth"] = bandwidth(w, q, attn_out, full_out, args)
+        result["bandwidth"] = _side("bandwidth", bandwidth, w, q, attn_out, full_out, args)
 
     if not args.no_selection:
-        result["selection"] = selection(w, args)
+        result["selection"] = _side("selection", selection, w, args)
 
     if not args.no_cache:
-        result["rolling_cache"] = rolling_cache(w, args)
+        result["rolling_cache"] = _side("rolling_cache", rolling_cache, w, args)
 
     if not args.no_frame_mask:
-        result["frame_mask"] = frame_mask(w, q, k, v, ws, args)
+        result["frame_mask"] = _side("frame_mask", frame_mask, w, q, k, v, ws, args)
 
     if not args.no_schedule:
-        result["schedule"] = schedule_loop(w, ws, args)
+        result["schedule"] = _side("schedule", schedule_loop, w, ws, args)
 
     if not args.no_shard:
-        result["head_shard"] = head_shard(w, args)
+        result["head_shard"] = _side("head_shard", head_shard, w, args)
 
     if not args.no_peaks:
-        result["measured_peaks"] = measured_peaks(attn_tflops)
+        result["measured_peaks"] = _side("measured_peaks", measured_peaks, attn_tflops)
 
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
+        result["cpu_baseline"] = _side("cpu_baseline", cpu_baseline, w, q, k, v, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
 
