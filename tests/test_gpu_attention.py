@@ -110,6 +110,23 @@ def test_one_token_per_frame():
     assert_parity(got, ref, "bf16", "N=1")
 
 
+def test_single_frame():
+    # T = 1: the only frame is the keyframe, S = N = 128 (two score blocks, one tile)
+    w = workloads.custom(1, 8, 16, 2, 128, (0,), dtype="bf16", seed=28)
+    got, ref, _ = _run_case(w)
+    assert_parity(got, ref, "bf16", "T=1")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_single_key_returns_v_exactly(dtype):
+    # S = 1: one key, p = 1 and l = 1 exactly, so every output row is its V row bit for bit
+    w = workloads.custom(1, 1, 1, 3, 64, (0,), dtype=dtype, seed=29)
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    out = rf.rf_keyframe_attention_ws(q, k, v, [0], w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    assert torch.equal(out, v)
+
+
 def test_many_heads_and_frames():
     w = workloads.custom(33, 3, 7, 24, 128, (0, 6, 12, 18, 24, 30, 31), dtype="bf16", seed=27)
     got, ref, _ = _run_case(w, rows=np.arange(0, w.M * w.N, 5))
