@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10,
                     help="untimed steps first (the clock takes a few hundred ms to settle under load)")
     ap.add_argument("--workload", default="long",
-                    help="long (default), 720p, 480p, small")
+                    help="long (default), 720p, 480p, small, tiny; the model shapes wan-1.3b, cogvideox")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--no-bandwidth", action="store_true")

@@ -20,8 +20,17 @@ normal draws with the shapes of those workloads:
            frame {0,6,...,30} plus 2 extra keyframes drawn with
            numpy.random.default_rng(4) from the remaining frames ({22, 31})
 
+Two more named shapes follow the paper's two models at their own sizes, with
+the paper's default of 4 keyframes (Sec. 4.1), evenly spaced:
+
+  wan-1.3b  T=21 x 45x80 (75,600 tokens), 12 heads, d=128, bf16 (Wan2.1-1.3B:
+            21 latent frames of 3,600 tokens), keyframes {0,7,13,20}
+  cogvideox T=11 x 48x85 (44,880 tokens), 48 heads, d=64, bf16 (CogVideoX-v1.5:
+            11 latent frames of 4,080 tokens; 48 heads of 64 in that model's
+            published configuration), keyframes {0,3,7,10}
+
 Draw order: Q, K, V from one torch generator seeded with the workload's index
-(tiny 0 ... long 4), fp32 randn, times the workload's scale, then rounded to
+(tiny 0 ... long 4, wan-1.3b 5, cogvideox 6), fp32 randn, times the workload's scale, then rounded to
 bf16 (round-to-nearest-even, torch's conversion) for the bf16 workloads.
 Latents: slot 0 then slot 1, fp32 randn from a generator seeded index + 100.
 Latent grids: tiny 4 x 5x16x16; 480p 16 x 21x60x104; the others 16 x T x 2H x 2W.
@@ -88,8 +97,13 @@ WORKLOADS = {
                      1.0, 16, (90, 160)),
     "long": Workload("long", 4, 33, 45, 80, 24, 128, "bf16", _long_video_keyframes(),
                      1.0, 16, (90, 160)),
+    "wan-1.3b": Workload("wan-1.3b", 5, 21, 45, 80, 12, 128, "bf16", (0, 7, 13, 20),
+                         1.0, 16, (90, 160)),
+    "cogvideox": Workload("cogvideox", 6, 11, 48, 85, 48, 64, "bf16", (0, 3, 7, 10),
+                          1.0, 16, (96, 170)),
 }
 ORDER = ["tiny", "small", "480p", "720p", "long"]
+MODEL_SHAPES = ["wan-1.3b", "cogvideox"]
 
 
 def custom(T, H, W, heads, head_dim, keyframes, dtype="bf16", seed=0,

@@ -202,7 +202,7 @@ def test_two_streams_are_ordered():
 # --- the workloads at full size, sampled rows -------------------------------------------
 
 @pytest.mark.parametrize("split", [False, True], ids=["whole", "split"])
-@pytest.mark.parametrize("name", ["small", "480p", "720p", "long"])
+@pytest.mark.parametrize("name", ["small", "480p", "720p", "long", "wan-1.3b", "cogvideox"])
 def test_workload_sampled_rows(name, split):
     w = workloads.WORKLOADS[name]
     rows = workloads.sample_rows(w, per_head=24 if w.heads > 12 else 48)

@@ -19,6 +19,8 @@ W = workloads.WORKLOADS
     ("480p", 21, 30, 52, 12, 128, "bf16"),
     ("720p", 21, 45, 80, 40, 128, "bf16"),
     ("long", 33, 45, 80, 24, 128, "bf16"),
+    ("wan-1.3b", 21, 45, 80, 12, 128, "bf16"),
+    ("cogvideox", 11, 48, 85, 48, 64, "bf16"),
 ])
 def test_shapes(name, T, H, Wd, heads, d, dtype):
     w = W[name]
@@ -36,11 +38,15 @@ def test_keyframe_sets_follow_the_stated_policies():
     assert base <= set(W["long"].keyframes) and len(extra) == 2
     assert extra == {22, 31}
     assert W["long"].M == 8
+    # the paper's two models with its default budget of 4 keyframes, evenly spaced
+    assert W["wan-1.3b"].keyframes == tuple(oracle.uniform_keyframes(21, 4)) == (0, 7, 13, 20)
+    assert W["cogvideox"].keyframes == tuple(oracle.uniform_keyframes(11, 4)) == (0, 3, 7, 10)
+    assert W["wan-1.3b"].N == 3600 and W["cogvideox"].N == 4080
 
 
 def test_small_workload_is_scaled():
     assert W["small"].qkv_scale == pytest.approx(1.0 / np.sqrt(128.0))
-    assert all(W[n].qkv_scale == 1.0 for n in ("tiny", "480p", "720p", "long"))
+    assert all(W[n].qkv_scale == 1.0 for n in ("tiny", "480p", "720p", "long", "wan-1.3b", "cogvideox"))
 
 
 def test_qkv_deterministic_shaped_and_scaled():
@@ -64,7 +70,7 @@ def test_latents_two_independent_slots():
     assert torch.equal(lat, workloads.make_latents(W["tiny"], B=2))
 
 
-@pytest.mark.parametrize("name", ["small", "long"])
+@pytest.mark.parametrize("name", ["small", "long", "cogvideox"])
 def test_sample_rows_cover_the_edges(name):
     w = W[name]
     rows = workloads.sample_rows(w, per_head=64)
