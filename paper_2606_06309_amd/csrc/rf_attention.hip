@@ -21,7 +21,7 @@
 //    the natural [key][dim] V tile with transposing LDS reads; the key order
 //    inside an operand follows the accumulator layout (a reduction index may
 //    be permuted freely as long as both operands agree).
-//  * K and V tiles of 64 keys go from HBM straight into LDS (buffer loads
+//  * K and V tiles (64 keys; 128 at head dimension 64) go from HBM straight into LDS (buffer loads
 //    with an LDS destination: no staging registers, no LDS write
 //    instructions), double-buffered so the next tile streams in while the
 //    current one is computed; the buffer range check zero-fills keys >= S and
@@ -43,7 +43,7 @@
 //    each part writes its unnormalised (O, m, l) in fp32, and a small kernel
 //    combines the parts of a tile (max of the references, rescaled sums).
 //  * Frame-level key/value mask (the kKvList form): the key loop walks a list
-//    of frames in 64-key tiles that never cross a frame; masked frames are
+//    of frames in key tiles that never cross a frame; masked frames are
 //    never read.
 // The fp32 kernel at the end is a plain correctness path (fp32 throughout).
 #include "rf_internal.h"
@@ -64,7 +64,7 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 // instruction that consumes them.
 
 // Tunables (compile-time): waves per workgroup (each owns 32 query rows), keys
-// per LDS tile, the largest row partial sum of a tile accepted before the
+// per LDS tile (at head dimension 128, and at 64), the largest row partial sum of a tile accepted before the
 // softmax reference is rebased (so every probability stays below it), and how
 // many LDS fragments the matrix core reads ahead.
 #ifndef RF_ATTN_WAVES
@@ -72,6 +72,9 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 #endif
 #ifndef RF_ATTN_BC
 #define RF_ATTN_BC 64
+#endif
+#ifndef RF_ATTN_BC64
+#define RF_ATTN_BC64 128
 #endif
 #ifndef RF_ATTN_REBASE_BOUND
 #define RF_ATTN_REBASE_BOUND 256.0f
@@ -86,7 +89,11 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 constexpr int kWaves = RF_ATTN_WAVES;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;   // query rows per workgroup
-constexpr int kBc = RF_ATTN_BC;    // keys per LDS tile
+// Keys per LDS tile. At head dimension 64 a tile of 64 keys carries half the
+// matrix work of one at 128 for the same softmax, barrier and loop overhead, so
+// it takes twice the keys (the registers and LDS that head dimension leaves free
+// hold them).
+__host__ __device__ constexpr int key_tile(int head_dim) { return head_dim == 64 ? RF_ATTN_BC64 : RF_ATTN_BC; }
 constexpr int kXcds = 8;
 // Split-key tail: compute units a round of whole tiles fills (one workgroup
 // per CU on MI355X), the most parts a tail tile is cut into, and the fewest
@@ -95,7 +102,7 @@ constexpr int kSplitCUs = 256;
 constexpr int kMaxSplit = 8;
 constexpr int kMinKvPerSplit = 8;
 constexpr float kRebaseBound = RF_ATTN_REBASE_BOUND;   // largest tile row sum kept without a rebase
-static_assert(kBc % 32 == 0, "key tile must be a multiple of 32");
+static_assert(key_tile(64) % 32 == 0 && key_tile(128) % 32 == 0, "key tile must be a multiple of 32");
 
 struct AttnKArgs {
     const uint16_t *q;
@@ -118,7 +125,7 @@ struct AttnKArgs {
     int32_t kf[kMaxFrames];
     // key/value frame list (frame-masked form only): the keys are the tokens
     // of frames kvf[0..n_kv), walked frame by frame in tiles that never cross
-    // a frame (tiles_per_frame = ceil(N / kBc); a frame's last tile is partial)
+    // a frame (tiles_per_frame = ceil(N / key tile); a frame's last tile is partial)
     int32_t n_kv;
     int32_t tiles_per_frame;
     int32_t kvf[kMaxFrames];
@@ -174,6 +181,7 @@ __device__ __forceinline__ float halves_sum(float x) {
 //      read pass (4 keys x 64 bytes) hit 8 different 32-byte positions.
 template <int D>
 struct TileLayout {
+    static constexpr int kBc = key_tile(D);            // keys per tile
     static constexpr int kRow = 2 * D;                 // bytes per key row
     static constexpr int kSlots = kRow / 16;           // 16-byte slots per row
     static constexpr int kRowsPerWin = 256 / kRow;     // rows per 256-byte bank window
@@ -292,6 +300,7 @@ template <int D, bool kKvList>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnKArgs a) {
     using L = TileLayout<D>;
+    constexpr int kBc = L::kBc;
     constexpr int kNB = kBc / 32;                       // 32-key score blocks per tile
     constexpr int kLoadsPerWave = L::kLoads / kWaves;
     static_assert(L::kLoads % kWaves == 0, "tile loads must split evenly over the waves");
@@ -709,6 +718,7 @@ __global__ __launch_bounds__(2 * kF32Rows) void attn_f32_kernel(const AttnF32Arg
 AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv) {
     AttnSplit sp{};
     const int64_t total = (Mq + kBr - 1) / kBr * heads;
+    const int64_t kBc = key_tile(head_dim);
     const int64_t kv_tiles = n_kv > 0 ? static_cast<int64_t>(n_kv) * ((N + kBc - 1) / kBc) : (S + kBc - 1) / kBc;
     const int64_t tail = total % kSplitCUs;
     sp.n_direct = total;
@@ -754,7 +764,8 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         const int64_t total = sp.n_direct;
         const int64_t per_xcd = (total + kXcds - 1) / kXcds;
         if (nq * p.heads > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
-        // per-lane load offsets inside a tile are 32-bit: kBc token rows must span < 2 GiB
+        // per-lane load offsets inside a tile are 32-bit: a tile's token rows must span < 2 GiB
+        const int64_t kBc = key_tile(p.head_dim);
         if (static_cast<int64_t>(p.heads) * p.head_dim * 2 * kBc >= 0x7fffffffLL) return hipErrorInvalidConfiguration;
         a.n_qtiles = static_cast<int32_t>(nq);
         a.total_tiles = static_cast<int32_t>(total);

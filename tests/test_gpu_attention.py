@@ -2,7 +2,8 @@
 
 All calls go through the C ABI (the ctypes binding). Element-by-element
 comparison on cases the oracle finishes in seconds that span several query
-tiles (128 rows) and key tiles (64 keys) with ragged tails; at the workloads'
+tiles (256 rows) and key tiles (64 keys at head dimension 128, 128 at 64) with
+ragged tails; at the workloads'
 full sizes, comparison on a seeded sample of rows (rows are independent, so
 the oracle is exact for every sampled row).
 """
@@ -55,7 +56,7 @@ def test_tiny_fp32_full():
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_ragged_multi_tile(d, dtype):
-    # N = 130 tokens per frame, S = 650 (S % 64 = 10), Mq = 390 (390 % 128 = 6)
+    # N = 130 tokens per frame, S = 650 (S % 64 = 10, S % 128 = 10), Mq = 390 (two query tiles, one partial)
     w = workloads.custom(5, 10, 13, 3, d, (0, 2, 4), dtype=dtype, seed=21)
     got, ref, _ = _run_case(w)
     assert_parity(got, ref, dtype, f"ragged d={d}")
@@ -241,7 +242,8 @@ SPLIT_CASES = [
     workloads.custom(8, 16, 16, 2, 128, (0, 5), dtype="bf16", seed=51),
     # ragged: 390 query rows (2 tiles per head, the second partial), 19 key tiles -> 2 parts
     workloads.custom(9, 10, 13, 3, 128, (0, 4, 8), dtype="bf16", seed=52),
-    workloads.custom(9, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=53),
+    # d = 64 (128-key tiles): 18 frames of 130 keys, 19 key tiles -> 2 parts
+    workloads.custom(18, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=53),
     # 3 frames of 40 x 52: 6,240 rows, 25 tiles per head, 4 heads -> 100 tiles, 98 key tiles -> 5 parts
     workloads.custom(3, 40, 52, 4, 128, (0, 1, 2), dtype="bf16", seed=54),
 ]
@@ -311,7 +313,9 @@ FRAME_SPLIT_CASES = [
     (workloads.custom(12, 16, 16, 2, 128, (0, 4, 8), dtype="bf16", seed=55), (0, 1, 2, 4, 5, 7, 8, 9, 10, 11)),
     # ragged frames of 130 keys (3 tiles, the last with 2 keys): 18 key tiles, parts start inside frames
     (workloads.custom(9, 10, 13, 3, 128, (0, 4, 8), dtype="bf16", seed=56), (0, 1, 3, 4, 6, 8)),
-    (workloads.custom(9, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=57), (1, 2, 3, 4, 5, 7, 8)),
+    # d = 64: frames of 130 keys in two 128-key tiles (the last with 2 keys), 26 key tiles
+    (workloads.custom(18, 10, 13, 3, 64, (1, 4, 7), dtype="bf16", seed=57),
+     (1, 2, 3, 4, 5, 7, 8, 10, 11, 13, 14, 16, 17)),
 ]
 
 

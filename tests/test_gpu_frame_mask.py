@@ -1,7 +1,7 @@
 """GPU parity of attention under a frame-level key/value mask
 (rf_frame_attention) against the oracle's frame_attention, through the C ABI:
 keyframe-only and other key/value frame lists on shapes whose frames are and
-are not multiples of the 64-key tile, every element; masked frames filled with
+are not multiples of the key tile, every element; masked frames filled with
 NaN (never read, so the output is unchanged bit for bit); the all-frames list
 equal to rf_keyframe_attention; sampled rows at 33 x 45 x 80, 24 heads."""
 import numpy as np
