@@ -172,6 +172,29 @@ def _stream(stream):
     return ctypes.c_void_p(int(stream))
 
 
+def _torch_stream(stream):
+    """The torch stream object of a launch stream argument (None: torch's
+    current stream, which needs no handling)."""
+    if stream is None or isinstance(stream, torch.cuda.Stream):
+        return stream
+    if int(stream) == 0:
+        return torch.cuda.default_stream()
+    return torch.cuda.ExternalStream(int(stream))
+
+
+def _empty(shape, dtype, device, stream):
+    """A tensor the call allocates for itself (an output or a workspace),
+    allocated while the launch stream is torch's current stream: the caching
+    allocator then ties the block to that stream, so once the tensor is dropped
+    the block is handed only to later work on the same stream, never to other
+    streams while the launch may still be using it."""
+    ts = _torch_stream(stream) if torch.device(device).type == "cuda" else None
+    if ts is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    with torch.cuda.stream(ts):
+        return torch.empty(shape, dtype=dtype, device=device)
+
+
 def _dev(t: torch.Tensor, name: str):
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
@@ -259,7 +282,7 @@ def rf_project_latents(latents: torch.Tensor, timesteps, keyframe_mask, out=None
         raise ValueError("latents must be [B][2][C][T][Hl][Wl]")
     B, _, C, T, Hl, Wl = latents.shape
     if out is None:
-        out = torch.empty((B, C, T, Hl, Wl), dtype=latents.dtype, device=latents.device)
+        out = _empty((B, C, T, Hl, Wl), latents.dtype, latents.device, stream)
     if out.dtype != latents.dtype or out.numel() != B * C * T * Hl * Wl:
         raise ValueError("out must match latents' dtype and [B][C][T][Hl][Wl] size")
     ts = (ctypes.c_double * 3)(*[float(x) for x in timesteps])
@@ -284,7 +307,7 @@ def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=Non
     ids, ids_p = _ids(keyframe_ids)
     M = ids.size
     if out is None:
-        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+        out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
     if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
         raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
     _check(lib.rf_keyframe_attention(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
@@ -302,9 +325,9 @@ def rf_attention_workspace(M: int, Mkv: int, T: int, H: int, W: int, heads: int,
     return int(n.value)
 
 
-def _workspace(workspace, nbytes, device):
+def _workspace(workspace, nbytes, device, stream):
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+        workspace = _empty(max(nbytes, 16), torch.uint8, device, stream)
     return workspace, workspace.numel() * workspace.element_size()
 
 
@@ -322,11 +345,11 @@ def rf_keyframe_attention_ws(q, k, v, keyframe_ids, T: int, H: int, W: int, out=
     ids, ids_p = _ids(keyframe_ids)
     M = ids.size
     if out is None:
-        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+        out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
     if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
         raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
     need = rf_attention_workspace(M, T, T, H, W, heads, d, q.dtype) if M > 0 else 0
-    workspace, wbytes = _workspace(workspace, need, q.device)
+    workspace, wbytes = _workspace(workspace, need, q.device, stream)
     _check(lib.rf_keyframe_attention_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                         ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
                                         _dev(workspace, "workspace"), wbytes, _stream(stream)))
@@ -349,7 +372,7 @@ def rf_frame_attention(q, k, v, q_frames, kv_frames, T: int, H: int, W: int, out
     kv, kv_p = _ids(kv_frames)
     M = ids.size
     if out is None:
-        out = torch.empty((M * H * W, heads, d), dtype=q.dtype, device=q.device)
+        out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
     if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
         raise ValueError("out must be [Mq*H*W][heads][head_dim] of q's dtype")
     ws_p, wbytes = (None, 0) if workspace is None else (_dev(workspace, "workspace"),
@@ -367,12 +390,12 @@ def rf_frame_similarity(latents: torch.Tensor, out=None, workspace=None, stream=
         raise ValueError("latents must be [B][C][T][H][W]")
     B, C, T, H, W = latents.shape
     if out is None:
-        out = torch.empty((B, T, T), dtype=torch.float64, device=latents.device)
+        out = _empty((B, T, T), torch.float64, latents.device, stream)
     if out.dtype != torch.float64 or out.numel() != B * T * T:
         raise ValueError("out must be float64 [B][T][T]")
     need = rf_frame_similarity_workspace(B, C, T, H, W)
     if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=latents.device)
+        workspace = _empty(max(need, 16), torch.uint8, latents.device, stream)
     _check(lib.rf_frame_similarity(_dev(latents, "latents"), _dev(out, "out"),
                                    _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
                                    B, C, T, H, W, _dtype_code(latents.dtype), _stream(stream)))
@@ -393,8 +416,8 @@ def rf_gather_frames(src_full: torch.Tensor, frame_ids, T: int, rows_per_frame: 
         raise ValueError("src_full must hold T * rows_per_frame rows")
     ids, ids_p = _ids(frame_ids)
     if out is None:
-        out = torch.empty((ids.size * rows_per_frame,) + tuple(src_full.shape[1:]),
-                          dtype=src_full.dtype, device=src_full.device)
+        out = _empty((ids.size * rows_per_frame,) + tuple(src_full.shape[1:]), src_full.dtype,
+                     src_full.device, stream)
     if out.numel() * out.element_size() != ids.size * rows_per_frame * row_bytes:
         raise ValueError("out must hold M * rows_per_frame rows")
     _check(lib.rf_gather_frames(_dev(src_full, "src_full"), _dev(out, "out"), ids_p, ids.size, T,
@@ -437,6 +460,25 @@ def _opt_dev(t, name):
     return None if t is None else _dev(t, name)
 
 
+def _check_h_full(h_full, code, nbytes):
+    """h_full holds all T frames' rows in the cache's dtype: exactly nbytes."""
+    if not isinstance(h_full, torch.Tensor):
+        raise TypeError("h_full must be a torch.Tensor")
+    if _dtype_code(h_full.dtype) != code:
+        raise TypeError(f"h_full has dtype {h_full.dtype}, the cache holds {'f32' if code == RF_F32 else 'bf16'}")
+    if h_full.numel() * h_full.element_size() != nbytes:
+        raise ValueError(f"h_full holds {h_full.numel() * h_full.element_size()} bytes, "
+                         f"T * rows_per_frame rows of the cache's row size are {nbytes}")
+
+
+def _check_store(store, need):
+    if not isinstance(store, torch.Tensor):
+        raise TypeError("store must be a torch.Tensor")
+    if store.numel() * store.element_size() < need:
+        raise ValueError(f"store is smaller than the cache needs ({store.numel() * store.element_size()} "
+                         f"of {need} bytes)")
+
+
 def rf_cache_init(frames, T: int, rows_per_frame: int, hidden: int, dtype, t_w: float,
                   store=None, h_full=None, cache=None, stream=None) -> rf_rolling_cache:
     """Sets up (or overwrites) `cache` for the listed frames at t_w and, when
@@ -444,6 +486,13 @@ def rf_cache_init(frames, T: int, rows_per_frame: int, hidden: int, dtype, t_w: 
     cache = rf_rolling_cache() if cache is None else cache
     ids, ids_p = _ids(frames)
     code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    if h_full is not None:
+        # the C ABI cannot see the buffers' sizes: check them here, before any launch
+        if store is None:
+            raise ValueError("h_full needs a store to copy into")
+        esize = 4 if code == RF_F32 else 2
+        _check_h_full(h_full, code, T * rows_per_frame * hidden * esize)
+        _check_store(store, rf_cache_store_bytes(ids.size, rows_per_frame, hidden, code))
     _check(lib.rf_cache_init(ctypes.byref(cache), _opt_dev(store, "store"), _opt_dev(h_full, "h_full"),
                              ids_p if ids.size else None, ids.size, T, rows_per_frame, hidden, code,
                              float(t_w), _stream(stream) if h_full is not None else None))
@@ -454,6 +503,11 @@ def rf_cache_shift_store(cache: rf_rolling_cache, t_denoise: float, store=None, 
                          frames=None, stream=None) -> rf_rolling_cache:
     """Shift-and-store at t_denoise for `frames` (None: every cached frame)."""
     _, ids_p, n = _frames_arg(frames)
+    if h_full is not None:
+        if store is None:
+            raise ValueError("h_full needs a store to copy into")
+        _check_h_full(h_full, cache.dtype, cache.T * cache.frame_bytes)
+        _check_store(store, 2 * cache.n_cached * cache.frame_bytes)
     _check(lib.rf_cache_shift_store(ctypes.byref(cache), _opt_dev(store, "store"),
                                     _opt_dev(h_full, "h_full"), ids_p, n, float(t_denoise),
                                     _stream(stream) if h_full is not None else None))
@@ -513,7 +567,7 @@ def rf_probe_mfma_bf16(operands: torch.Tensor, workgroups: int, rounds: int, sin
     if operands.dtype != torch.bfloat16 or operands.numel() != 12 * 64 * 8:
         raise ValueError("operands must be bf16 with 12 * 64 * 8 elements")
     if sink is None:
-        sink = torch.empty(workgroups * PROBE_THREADS, dtype=torch.float32, device=operands.device)
+        sink = _empty(workgroups * PROBE_THREADS, torch.float32, operands.device, stream)
     if sink.dtype != torch.float32 or sink.numel() < workgroups * PROBE_THREADS:
         raise ValueError("sink must be float32 with workgroups * 256 elements")
     _check(lib.rf_probe_mfma_bf16(_dev(operands, "operands"), workgroups, rounds, _dev(sink, "sink"),
@@ -525,7 +579,7 @@ def rf_probe_hbm_read(src: torch.Tensor, workgroups: int, sink=None, stream=None
     """Enqueues the HBM read probe over src's bytes; returns the sink, int32
     [workgroups * 256] whose XOR is the XOR of src's 32-bit words."""
     if sink is None:
-        sink = torch.empty(workgroups * PROBE_THREADS, dtype=torch.int32, device=src.device)
+        sink = _empty(workgroups * PROBE_THREADS, torch.int32, src.device, stream)
     if sink.element_size() != 4 or sink.numel() < workgroups * PROBE_THREADS:
         raise ValueError("sink must have 4-byte elements, workgroups * 256 of them")
     _check(lib.rf_probe_hbm_read(_dev(src, "src"), src.numel() * src.element_size(), workgroups,

@@ -50,3 +50,49 @@ def test_non_contiguous_is_rejected_before_the_device_check():
 def test_probe_operand_shape_is_checked():
     with pytest.raises(ValueError, match="12 \\* 64 \\* 8"):
         rf.rf_probe_mfma_bf16(torch.zeros((16, 64, 8), dtype=torch.bfloat16), 1, 1)
+
+
+# --- the rolling cache's buffers: sizes and dtypes checked before any launch --------
+
+NK = [1, 2]            # cached frames of a T = 3 video, 16 rows of 128 elements each
+ROWS, HID = H * W, HEADS * D
+
+
+def _h(T_=T, dtype=torch.bfloat16, rows=ROWS):
+    return torch.zeros((T_ * rows, HID), dtype=dtype)
+
+
+def _store(n_frames=len(NK), dtype=torch.bfloat16):
+    return torch.zeros((2 * n_frames * ROWS, HID), dtype=dtype)
+
+
+@pytest.mark.parametrize("bad,err,match", [
+    (dict(store=_store(1)), ValueError, "store is smaller"),
+    (dict(h_full=_h(T_=T - 1)), ValueError, "h_full holds"),
+    (dict(h_full=_h(dtype=torch.float32)), TypeError, "dtype"),
+    (dict(store=None), ValueError, "needs a store"),
+])
+def test_cache_init_checks_buffers(bad, err, match):
+    args = dict(store=_store(), h_full=_h())
+    args.update(bad)
+    with pytest.raises(err, match=match):
+        rf.rf_cache_init(NK, T, ROWS, HID, torch.bfloat16, 10.0, **args)
+
+
+def test_cache_init_right_sizes_reach_the_device_check():
+    with pytest.raises(ValueError, match="device"):
+        rf.rf_cache_init(NK, T, ROWS, HID, torch.bfloat16, 10.0, store=_store(), h_full=_h())
+
+
+@pytest.mark.parametrize("bad,err,match", [
+    (dict(store=_store(1)), ValueError, "store is smaller"),
+    (dict(h_full=torch.zeros((T * ROWS + 1, HID), dtype=torch.bfloat16)), ValueError, "h_full holds"),
+    (dict(h_full=_h(dtype=torch.float32)), TypeError, "dtype"),
+])
+def test_cache_shift_store_checks_buffers(bad, err, match):
+    cache = rf.rf_cache_init(NK, T, ROWS, HID, torch.bfloat16, 10.0)   # bookkeeping only, no copy
+    args = dict(store=_store(), h_full=_h())
+    args.update(bad)
+    with pytest.raises(err, match=match):
+        rf.rf_cache_shift_store(cache, 8.0, **args)
+    assert cache.t_after[1] == 10.0   # nothing changed

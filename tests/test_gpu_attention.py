@@ -85,6 +85,77 @@ def test_peaked_softmax_relative(d):
     assert_parity(got / s, ref / s, "bf16", "peaked (scaled)")
 
 
+def _late_rebase_rows(q, k, keyframes, N, head_dim):
+    """Lower bound on the query rows whose softmax reference must move after
+    the first key tile: the kernel takes probabilities against a past row
+    maximum and rebases when a tile's row sum exceeds 256, which is certain
+    once one score of the tile exceeds the reference by more than 8 in the
+    log2 domain. Computed per (row, head) from the exact scores; returns the
+    fraction of (row, head) pairs with at least one such tile past the first."""
+    qh, kh = torch_bf16_to_f64(q), torch_bf16_to_f64(k)
+    rows = oracle.rowmap(keyframes, N)
+    bc = 128 if head_dim == 64 else 64
+    S, heads = kh.shape[0], kh.shape[1]
+    hits = total = 0
+    for h in range(heads):
+        s = qh[rows, h] @ kh[:, h].T * (math.log2(math.e) / math.sqrt(head_dim))
+        ntiles = -(-S // bc)
+        tmax = np.stack([s[:, t * bc:(t + 1) * bc].max(axis=1) for t in range(ntiles)], axis=1)
+        ref = tmax[:, 0].copy()
+        late = np.zeros(len(rows), dtype=bool)
+        for t in range(1, ntiles):
+            jump = tmax[:, t] > ref + 8.05
+            late |= jump
+            ref = np.where(jump, tmax[:, t], ref)
+        hits += int(late.sum())
+        total += len(rows)
+    return hits / total
+
+
+# (T, H, W, keyframes) spanning >= 10 key tiles at each head dimension: d = 128
+# has 64-key tiles (1,600 keys: 25 tiles), d = 64 has 128-key tiles (2,400 keys:
+# 19 tiles); 600 query rows in 3 query tiles, the last partial.
+SHARP_SHAPES = {128: (8, 10, 20, (0, 3, 6)), 64: (12, 10, 20, (0, 5, 11))}
+
+
+def _sharp_case(d, seed, k_ramp):
+    T, H, W, kf = SHARP_SHAPES[d]
+    w = workloads.custom(T, H, W, 2, d, kf, dtype="bf16", seed=seed)
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    q = (q.float() * 4.0).to(torch.bfloat16)
+    if k_ramp:
+        ramp = 0.25 + torch.arange(w.S, device="cuda", dtype=torch.float32) / w.S
+        k = (k.float() * ramp[:, None, None]).to(torch.bfloat16)
+    return w, q.contiguous(), k.contiguous(), v
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["whole", "split"])
+@pytest.mark.parametrize("k_ramp", [False, True], ids=["plain", "late_maxima"])
+@pytest.mark.parametrize("d", [64, 128])
+def test_sharp_softmax_absolute(d, k_ramp, split):
+    """The sharp case under the absolute bf16 gates: Q x 4 with K and V
+    unscaled (logit std ~ 4, outputs |O| <= ~4 stay O(1)), so the online
+    softmax's reference has to move in later key tiles. "late_maxima" also
+    scales K by a ramp 0.25 -> 1.25 along the keys, so every row's maxima sit in
+    later tiles and every row rebases there. Asserted on the CPU before the
+    comparison: the inputs force a rebase past the first key tile in at least
+    10 % (plain) / all (late_maxima) of the (row, head) pairs."""
+    w, q, k, v = _sharp_case(d, 61 + d, k_ramp)
+    print(f"[case] sharp absolute d={d} S={w.S} ramp={k_ramp} split={split}", flush=True)
+    frac = _late_rebase_rows(q.cpu(), k.cpu(), w.keyframes, w.N, d)
+    assert frac >= (1.0 if k_ramp else 0.10), f"only {frac:.3f} of rows rebase past the first tile"
+    if split:
+        assert rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, d, rf.RF_BF16) > 0
+        out = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W)
+    else:
+        out = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    ref = oracle.keyframe_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, w.N)
+    assert 1.0 < float(np.abs(ref).max()) < 8.0
+    st = assert_parity(_to_f64(out), ref, "bf16", f"sharp absolute d={d} ramp={k_ramp} split={split}")
+    print(f"[parity] sharp d={d} ramp={k_ramp} split={split}: late-rebase rows {frac:.3f}, {st}", flush=True)
+
+
 def test_near_uniform_small_scale():
     w = workloads.custom(7, 12, 14, 2, 128, (0, 3, 6), dtype="bf16", seed=23,
                          qkv_scale=1.0 / math.sqrt(128.0))
@@ -198,6 +269,42 @@ def test_two_streams_are_ordered():
         rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W, out=out2, stream=s2)
     torch.cuda.synchronize()
     assert torch.equal(out1, ref) and torch.equal(out2, ref)
+
+
+# --- the small workload, every row of two heads -------------------------------------------
+
+SMALL_FULL_HEADS = (0, 11)
+
+
+@pytest.fixture(scope="module")
+def small_full():
+    """The small workload (13 frames of 30 x 52, 12 heads, keyframes every 3rd
+    frame, inputs scaled by 1/sqrt(128)) and the oracle on every query row of
+    heads 0 and 11: 7,800 rows x 20,280 keys each. Its 372 tiles run as one full
+    round of 256 whole tiles plus 116 tail tiles (heads 8-11), so with the
+    workspace head 0 runs whole and head 11 in key parts."""
+    w = workloads.WORKLOADS["small"]
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    print(f"[case] small every row of heads {SMALL_FULL_HEADS}: oracle ...", flush=True)
+    ref = oracle.keyframe_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, w.N, heads=list(SMALL_FULL_HEADS))
+    return w, (q, k, v), ref
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["whole", "split"])
+def test_small_workload_every_row_of_two_heads(small_full, split):
+    w, (q, k, v), ref = small_full
+    print(f"[case] small every row heads={SMALL_FULL_HEADS} split={split}", flush=True)
+    if split:
+        assert rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, rf.RF_BF16) > 0
+        out = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W)
+    else:
+        out = rf.rf_keyframe_attention(q, k, v, w.keyframes, w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    got = _to_f64(out)[:, list(SMALL_FULL_HEADS)]
+    assert got.shape == (w.M * w.N, 2, w.head_dim)
+    for i, h in enumerate(SMALL_FULL_HEADS):
+        st = assert_parity(got[:, i], ref[:, i], "bf16", f"small head {h} split={split}")
+        print(f"[parity] small head {h} split={split}: {st}", flush=True)
 
 
 # --- the workloads at full size, sampled rows -------------------------------------------
@@ -332,3 +439,26 @@ def test_frame_attention_split_tail(case):
     torch.cuda.synchronize()
     ref = oracle.frame_attention(q.cpu(), k.cpu(), v.cpu(), w.keyframes, kvf, w.N)
     assert_parity(_to_f64(out), ref, "bf16", "frame mask split tail")
+
+
+def test_internal_workspace_on_a_side_stream():
+    """rf_keyframe_attention_ws launched on a side stream with a workspace the
+    binding allocates (and drops on return) while the current stream keeps
+    allocating and writing NaN: the workspace belongs to the side stream's
+    pool, so the current stream's allocations never receive it mid-launch and
+    every output equals the current-stream result bit for bit."""
+    w = SPLIT_CASES[3]
+    assert _split_plan(w) > 0
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    ref = rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    outs = [torch.empty_like(ref) for _ in range(4)]
+    torch.cuda.synchronize()
+    for o in outs:
+        rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, out=o, stream=side)
+        junk = torch.full((_split_plan(w) // 4 + 4096,), float("nan"), device="cuda")
+        del junk
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o, ref)

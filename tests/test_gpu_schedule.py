@@ -11,7 +11,13 @@ own (fp64, never fed from the GPU):
     cache:  the non-keyframes' keys and values come from the per-layer rolling
       cache (App. B.2): initialised from the last warm-up step's output,
       shift-and-store at each Rhythmic Point, projected into K and V before the
-      keyframe-query attention.
+      keyframe-query attention. Each stored state is labelled with the step it
+      was computed at, so every later skipped step lies below the newest label
+      and the appendix's weight clamps to 1 (the cache returns h_after).
+    cache_interp: as cache, but each stored state is labelled with the time its
+      update leads the non-keyframes to (the plan's target time): the skipped
+      steps then lie strictly inside (t_after, t_before) and are interpolated
+      with 0 < alpha < 1, which the test asserts at every skipped step.
 
 Every step's whole output is compared with the oracle's under the attention
 gates. In the cache form a step's output feeds later steps through the cache;
@@ -63,7 +69,7 @@ def test_plan_matches_the_oracle_plan():
             assert p["alpha"] == pytest.approx(r["alpha"], abs=1e-15)
 
 
-@pytest.mark.parametrize("mode", ["latent", "cache"])
+@pytest.mark.parametrize("mode", ["latent", "cache", "cache_interp"])
 @pytest.mark.parametrize("w,kind", CASES, ids=lambda x: getattr(x, "name", None) and f"{x.name}_N{x.N}_d{x.head_dim}")
 def test_schedule_step_by_step(w, kind, mode):
     print(f"[case] schedule {PLAN} {mode} {w.name} T={w.T} N={w.N} d={w.head_dim} {kind}", flush=True)
@@ -86,6 +92,7 @@ def test_schedule_step_by_step(w, kind, mode):
     cache = cache_ref = None
     nonkey_rows = np.concatenate([np.arange(f * w.N, (f + 1) * w.N) for f in nonkey])
     projections = 0
+    alphas = []
     for i, step in enumerate(plan):
         q, k, v = sets[i % 2]
         qr, kr, vr = sets_ref[i % 2]
@@ -93,20 +100,30 @@ def test_schedule_step_by_step(w, kind, mode):
         if step["phase"] != "skip":
             rf.rf_keyframe_attention(q, k, v, list(range(w.T)), w.T, w.H, w.W, out=full_out)
             full_ref = oracle.keyframe_attention(qr, kr, vr, list(range(w.T)), w.N)
-            if mode == "cache":
+            if mode != "latent":
                 last_warmup = step["phase"] == "warmup" and (i + 1 == len(plan) or plan[i + 1]["phase"] != "warmup")
                 h_ref = full_ref.reshape(w.T, w.N, D)
+                label = float(step["nonkey_to"] if mode == "cache_interp" else step["t"])
                 if last_warmup:
-                    cache = rf.rf_cache_init(nonkey, w.T, w.N, D, w.torch_dtype, float(step["t"]), store=store,
+                    cache = rf.rf_cache_init(nonkey, w.T, w.N, D, w.torch_dtype, label, store=store,
                                              h_full=full_out)
                     cache_ref = oracle.RollingCache()
-                    cache_ref.init(nonkey, {f: h_ref[f] for f in nonkey}, float(step["t"]))
+                    cache_ref.init(nonkey, {f: h_ref[f] for f in nonkey}, label)
                 elif step["phase"] == "rhythmic":
-                    rf.rf_cache_shift_store(cache, float(step["t"]), store=store, h_full=full_out)
-                    cache_ref.shift_and_store(nonkey, {f: h_ref[f] for f in nonkey}, float(step["t"]))
+                    rf.rf_cache_shift_store(cache, label, store=store, h_full=full_out)
+                    cache_ref.shift_and_store(nonkey, {f: h_ref[f] for f in nonkey}, label)
         else:
             before = _bits(full_out)
-            if mode == "cache":
+            if mode != "latent":
+                for f in nonkey:
+                    a = rf.rf_cache_alpha(cache, f, float(step["t"]))
+                    a_ref = oracle.hidden_alpha(cache_ref.t_before[f], cache_ref.t_after[f], float(step["t"]))
+                    assert a == pytest.approx(a_ref, abs=1e-15), what
+                    if mode == "cache_interp":
+                        assert 0.0 < a < 1.0, f"{what}: alpha {a} of frame {f} is not interior"
+                        alphas.append(a)
+                    else:
+                        assert a == 1.0, what
                 k, v = k.clone(), v.clone()
                 rf.rf_cache_project_kv(cache, store, k, v, float(step["t"]))
                 kr, vr = oracle.skip_step_kv(kr, vr, cache_ref, nonkey, float(step["t"]), w.N)
@@ -129,3 +146,7 @@ def test_schedule_step_by_step(w, kind, mode):
         assert_parity(_f64(full_out), full_ref, kind, what)
     assert cache is not None or mode == "latent"
     assert projections == (6 if mode == "latent" else 0)
+    if mode == "cache_interp":
+        # the plan's skipped steps: 9 and 7 (alpha 1/2), 5, 4, 2, 1 (alpha 1/3, 2/3)
+        assert len(alphas) == 6 * len(nonkey)
+        assert sorted(set(round(a, 6) for a in alphas)) == [round(1 / 3, 6), 0.5, round(2 / 3, 6)]
