@@ -21,7 +21,10 @@
  *    this ABI. rf_last_error() gives a thread-local description of the last
  *    failure on the calling thread.
  *  - Every argument is validated before any HIP call, so a rejected call has
- *    no effect on the device.
+ *    no effect on the device. The one HIP call that may come first is a query
+ *    of the current device's compute-unit and XCD counts (bf16 attention and
+ *    the plan queries with compute_units = 0), made once per device; a failed
+ *    query returns RF_ERR_HIP.
  *  - Device buffers are owned by the caller, must stay alive until the stream
  *    has passed the launched work, and are never retained by the library.
  *    Host arrays are read during the call only; the caller may free them when
@@ -31,7 +34,8 @@
  *  - `stream` is a hipStream_t (NULL = the default stream). Calls only enqueue
  *    work; they do not synchronise. Device faults surface at the caller's next
  *    synchronisation, not as a return code.
- *  - Calls hold no global state and may be made from several threads.
+ *  - Calls may be made from several threads. The only state kept between
+ *    calls is the per-device geometry above (read-only once queried).
  *  - Device pointers must be 16-byte aligned (128-bit accesses), otherwise
  *    RF_ERR_UNSUPPORTED, unless a call states a weaker requirement.
  */
@@ -44,11 +48,14 @@
 extern "C" {
 #endif
 
-#define RF_ABI_VERSION 1
+#define RF_ABI_VERSION 2
 
 /* Largest number of frames T a call accepts (keyframe ids travel inside the
    kernel arguments, which needs no device copy and no allocation). */
 #define RF_MAX_FRAMES 256
+
+/* Largest compute-unit count an attention plan query accepts. */
+#define RF_MAX_COMPUTE_UNITS 65536
 
 typedef enum {
     RF_OK = 0,
@@ -167,7 +174,8 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
 /*
  * rf_keyframe_attention with a caller workspace for a split-key tail: one
  * bf16 workgroup of 256 query rows fills a compute unit, so ceil(M*N/256)*heads
- * workgroups run in whole rounds of 256; the tiles beyond the last full round
+ * workgroups run in whole rounds of the device's compute units (256 on
+ * MI355X); the tiles beyond the last full round
  * are cut along the keys into parts that run side by side, and a second small
  * kernel combines each tile's parts (max of the parts' reference maxima,
  * rescaled sums, one bf16 rounding). Rows of split tiles differ from the
@@ -176,7 +184,8 @@ int rf_keyframe_attention(const void *q, const void *k, const void *v, void *out
  * of different M that rf_keyframe_attention has does not hold here.
  *
  * workspace: device, 16-byte aligned, at least rf_attention_workspace bytes
- *   (may be 0: then nothing is split), not overlapping q, k, v or out; its
+ *   for the current device's compute units (compute_units = 0 there) (may be
+ *   0: then nothing is split), not overlapping q, k, v or out; its
  *   contents are overwritten and meaningless afterwards. fp32 ignores it.
  * Other arguments and errors as rf_keyframe_attention; RF_ERR_INVALID_ARG also
  * for a NULL or too small workspace or an overlap.
@@ -188,14 +197,40 @@ int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *
 
 /*
  * Bytes of workspace rf_keyframe_attention_ws (Mkv = T) or rf_frame_attention
- * (Mkv key/value frames) uses for these sizes (host only; 0 when nothing is
- * split, always 0 for RF_F32). The split assumes MI355X's 256 compute units.
- * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (T, M, Mkv, sizes
- *         whose byte counts would pass 4e18),
- * RF_ERR_UNSUPPORTED (head_dim, dtype).
+ * (Mkv key/value frames) uses for these sizes on a device of compute_units
+ * compute units (0 when nothing is split, always 0 for RF_F32). The split-key
+ * tail fills the compute units a round of whole tiles leaves idle, so the plan
+ * depends on their number: the launch uses the current device's count.
+ * compute_units: 1..RF_MAX_COMPUTE_UNITS (host only, no HIP call), or 0 for the
+ *   current device's count (queried once per device; 256 on MI355X).
+ * Errors: RF_ERR_INVALID_ARG (NULL, sizes <= 0), RF_ERR_RANGE (T, M, Mkv,
+ *         compute_units, sizes whose byte counts would pass 4e18),
+ *         RF_ERR_UNSUPPORTED (head_dim, dtype), RF_ERR_HIP (compute_units = 0
+ *         and no device to query).
  */
 int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
-                           int32_t head_dim, int32_t dtype, int64_t *bytes_out);
+                           int32_t head_dim, int32_t dtype, int32_t compute_units, int64_t *bytes_out);
+
+/* How a bf16 attention launch is cut (rf_attention_plan). A tile is 256 query
+   rows of one head and runs as one workgroup filling one compute unit. */
+typedef struct rf_attention_split {
+    int64_t tiles;              /* ceil(M*N / 256) * heads */
+    int64_t whole_tiles;        /* tiles computed over all keys in one workgroup */
+    int64_t tail_tiles;         /* tiles past the last full round, cut along the keys */
+    int32_t parts;              /* parts per tail tile (0: nothing is split) */
+    int32_t key_tiles_per_part; /* key tiles per part (64 keys each; 128 at head_dim 64) */
+    int64_t workspace_bytes;    /* tail_tiles * parts * 256 * (4 * head_dim + 8) */
+    int32_t compute_units;      /* the count the plan is made for */
+    int32_t reserved;
+} rf_attention_split;
+
+/*
+ * The split plan rf_keyframe_attention_ws / rf_frame_attention use for these
+ * sizes on compute_units compute units (arguments and errors as
+ * rf_attention_workspace). For RF_F32 every count is 0 (no split).
+ */
+int rf_attention_plan(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                      int32_t dtype, int32_t compute_units, rf_attention_split *plan_out);
 
 /*
  * Attention under a frame-level key/value mask: the frame mask M_Rhyme (in

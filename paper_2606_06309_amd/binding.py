@@ -31,6 +31,7 @@ EXPORTED = [
     "rf_status_string", "rf_last_error", "rf_abi_version",
     "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
     "rf_project_latents", "rf_keyframe_attention", "rf_keyframe_attention_ws", "rf_attention_workspace",
+    "rf_attention_plan",
     "rf_frame_attention",
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
@@ -76,6 +77,20 @@ class rf_rolling_cache(ctypes.Structure):
     ]
 
 
+class rf_attention_split(ctypes.Structure):
+    """The C struct rf_attention_split (how a bf16 attention launch is cut)."""
+    _fields_ = [
+        ("tiles", ctypes.c_int64),
+        ("whole_tiles", ctypes.c_int64),
+        ("tail_tiles", ctypes.c_int64),
+        ("parts", ctypes.c_int32),
+        ("key_tiles_per_part", ctypes.c_int32),
+        ("workspace_bytes", ctypes.c_int64),
+        ("compute_units", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
 class RhymeFlowError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{message} [{status}]")
@@ -118,8 +133,11 @@ lib.rf_frame_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32p, _i32,
 lib.rf_keyframe_attention_ws.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
                                          _i32, _i32, _i32, _vp, _i64, _vp]
 lib.rf_keyframe_attention_ws.restype = ctypes.c_int
-lib.rf_attention_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64)]
+lib.rf_attention_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64)]
 lib.rf_attention_workspace.restype = ctypes.c_int
+lib.rf_attention_plan.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                  ctypes.POINTER(rf_attention_split)]
+lib.rf_attention_plan.restype = ctypes.c_int
 lib.rf_frame_attention.restype = ctypes.c_int
 lib.rf_gather_frames.argtypes = [_vp, _vp, _i32p, _i32, _i32, _i64, _i64, _vp]
 lib.rf_gather_frames.restype = ctypes.c_int
@@ -316,13 +334,25 @@ def rf_keyframe_attention(q, k, v, keyframe_ids, T: int, H: int, W: int, out=Non
     return out
 
 
-def rf_attention_workspace(M: int, Mkv: int, T: int, H: int, W: int, heads: int, head_dim: int, dtype) -> int:
+def rf_attention_workspace(M: int, Mkv: int, T: int, H: int, W: int, heads: int, head_dim: int, dtype,
+                           compute_units: int = 0) -> int:
     """Bytes of split-tail workspace rf_keyframe_attention_ws (Mkv = T) or
-    rf_frame_attention uses (0: nothing is split)."""
+    rf_frame_attention uses (0: nothing is split) on a device of compute_units
+    compute units (0: the current device, which the launch uses)."""
     n = _i64(0)
     code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
-    _check(lib.rf_attention_workspace(M, Mkv, T, H, W, heads, head_dim, code, ctypes.byref(n)))
+    _check(lib.rf_attention_workspace(M, Mkv, T, H, W, heads, head_dim, code, compute_units, ctypes.byref(n)))
     return int(n.value)
+
+
+def rf_attention_plan(M: int, Mkv: int, T: int, H: int, W: int, heads: int, head_dim: int, dtype,
+                      compute_units: int = 0) -> dict:
+    """The split plan of a bf16 attention launch as a dict of the fields of
+    rf_attention_split (compute_units 0: the current device)."""
+    p = rf_attention_split()
+    code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    _check(lib.rf_attention_plan(M, Mkv, T, H, W, heads, head_dim, code, compute_units, ctypes.byref(p)))
+    return {name: int(getattr(p, name)) for name, _ in rf_attention_split._fields_ if name != "reserved"}
 
 
 def _workspace(workspace, nbytes, device, stream):
@@ -348,10 +378,10 @@ def rf_keyframe_attention_ws(q, k, v, keyframe_ids, T: int, H: int, W: int, out=
         out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
     if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
         raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
-    need = rf_attention_workspace(M, T, T, H, W, heads, d, q.dtype) if M > 0 else 0
+    ptrs = [_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out")]
+    need = rf_attention_workspace(M, T, T, H, W, heads, d, q.dtype) if M > 0 and workspace is None else 0
     workspace, wbytes = _workspace(workspace, need, q.device, stream)
-    _check(lib.rf_keyframe_attention_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
-                                        ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
+    _check(lib.rf_keyframe_attention_ws(*ptrs, ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
                                         _dev(workspace, "workspace"), wbytes, _stream(stream)))
     return out
 

@@ -197,12 +197,21 @@ int rf_project_latents(const void *latents, void *out, const double timesteps[3]
 }
 
 // Shared validation and launch of the two attention entry points.
-// Bytes of split-tail workspace a bf16 attention of these sizes uses (0 for fp32
-// or when nothing is split); the sizes must already be valid.
+// Bytes of split-tail workspace a bf16 attention of these sizes uses on a device
+// of `cus` compute units (0 for fp32 or when nothing is split); the sizes must
+// already be valid.
 static int64_t attention_ws_need(int32_t M, int32_t n_kv, int32_t T, int64_t N, int32_t heads, int32_t head_dim,
-                                 int32_t dtype) {
+                                 int32_t dtype, int32_t cus) {
     if (dtype != RF_BF16) return 0;
-    return rf::attention_split(static_cast<int64_t>(M) * N, heads, head_dim, N, N * T, n_kv).ws_bytes;
+    return rf::attention_split(static_cast<int64_t>(M) * N, heads, head_dim, N, N * T, n_kv, cus).ws_bytes;
+}
+
+// The current device's geometry, as an rf_status.
+static int query_geometry(rf::DeviceGeometry *geo, const char *fn) {
+    const hipError_t e = rf::device_geometry(geo);
+    if (e != hipSuccess)
+        return fail(RF_ERR_HIP, "%s: cannot query the current device: %s", fn, hipGetErrorString(e));
+    return RF_OK;
 }
 
 static int attention_call(const void *q, const void *k, const void *v, void *out, const int32_t *q_ids,
@@ -241,14 +250,23 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
         return fail(RF_ERR_INVALID_ARG, "%s: out overlaps q, k or v", fn);
     const int32_t n_kv = (kv_ids && Mkv < T) ? Mkv : 0;
     if (ws) {
-        const int64_t need = attention_ws_need(M, n_kv, T, N, heads, head_dim, dtype);
-        if (ws_bytes < need)
-            return fail(RF_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed", fn,
-                        static_cast<long long>(ws_bytes), static_cast<long long>(need));
+        if (ws_bytes < 0) return fail(RF_ERR_INVALID_ARG, "%s: workspace_bytes < 0", fn);
         if (!aligned16(ws)) return fail(RF_ERR_UNSUPPORTED, "%s: workspace must be 16-byte aligned", fn);
-        if (need > 0 && (overlaps(ws, need, q, in_bytes) || overlaps(ws, need, k, in_bytes) ||
-                         overlaps(ws, need, v, in_bytes) || overlaps(ws, need, out, out_bytes)))
+        if (ws_bytes > 0 && (overlaps(ws, ws_bytes, q, in_bytes) || overlaps(ws, ws_bytes, k, in_bytes) ||
+                             overlaps(ws, ws_bytes, v, in_bytes) || overlaps(ws, ws_bytes, out, out_bytes)))
             return fail(RF_ERR_INVALID_ARG, "%s: workspace overlaps q, k, v or out", fn);
+    }
+    // every argument is valid: the bf16 split plan and tile order follow the device
+    p.geo.cus = p.geo.xcds = 1;
+    if (dtype == RF_BF16) {
+        rc = query_geometry(&p.geo, fn);
+        if (rc != RF_OK) return rc;
+    }
+    if (ws) {
+        const int64_t need = attention_ws_need(M, n_kv, T, N, heads, head_dim, dtype, p.geo.cus);
+        if (ws_bytes < need)
+            return fail(RF_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed on %d compute units", fn,
+                        static_cast<long long>(ws_bytes), static_cast<long long>(need), p.geo.cus);
         p.ws = need > 0 ? ws : nullptr;
         p.ws_bytes = ws_bytes;
     }
@@ -297,10 +315,10 @@ int rf_frame_attention(const void *q, const void *k, const void *v, void *out,
                           workspace, workspace_bytes, stream, fn);
 }
 
-int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
-                           int32_t head_dim, int32_t dtype, int64_t *bytes_out) {
-    const char *fn = "rf_attention_workspace";
-    if (!bytes_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+// Sizes of an attention plan query, and the compute units it is planned for
+// (0: the current device's, which needs a device query).
+static int plan_args(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                     int32_t dtype, int32_t compute_units, int32_t *cus, const char *fn) {
     if (H <= 0 || W <= 0 || heads <= 0 || T <= 0 || M <= 0 || Mkv <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
     if (T > RF_MAX_FRAMES) return fail(RF_ERR_RANGE, "%s: T = %d exceeds %d", fn, T, RF_MAX_FRAMES);
@@ -310,7 +328,53 @@ int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t
     if (dtype != RF_BF16 && dtype != RF_F32) return fail(RF_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
     if (static_cast<double>(H) * W * T * heads * head_dim * 4.0 > kMaxBytes)
         return fail(RF_ERR_RANGE, "%s: sizes overflow 64-bit byte counts", fn);
-    *bytes_out = attention_ws_need(M, Mkv < T ? Mkv : 0, T, static_cast<int64_t>(H) * W, heads, head_dim, dtype);
+    if (compute_units < 0 || compute_units > RF_MAX_COMPUTE_UNITS)
+        return fail(RF_ERR_RANGE, "%s: compute_units = %d outside 0..%d", fn, compute_units, RF_MAX_COMPUTE_UNITS);
+    if (compute_units > 0) {
+        *cus = compute_units;
+        return RF_OK;
+    }
+    rf::DeviceGeometry geo;
+    const int rc = query_geometry(&geo, fn);
+    if (rc != RF_OK) return rc;
+    *cus = geo.cus;
+    return RF_OK;
+}
+
+int rf_attention_workspace(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads,
+                           int32_t head_dim, int32_t dtype, int32_t compute_units, int64_t *bytes_out) {
+    const char *fn = "rf_attention_workspace";
+    if (!bytes_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    int32_t cus = 0;
+    const int rc = plan_args(M, Mkv, T, H, W, heads, head_dim, dtype, compute_units, &cus, fn);
+    if (rc != RF_OK) return rc;
+    *bytes_out = attention_ws_need(M, Mkv < T ? Mkv : 0, T, static_cast<int64_t>(H) * W, heads, head_dim, dtype,
+                                   cus);
+    return ok();
+}
+
+int rf_attention_plan(int32_t M, int32_t Mkv, int32_t T, int32_t H, int32_t W, int32_t heads, int32_t head_dim,
+                      int32_t dtype, int32_t compute_units, rf_attention_split *plan_out) {
+    const char *fn = "rf_attention_plan";
+    if (!plan_out) return fail(RF_ERR_INVALID_ARG, "%s: NULL output", fn);
+    int32_t cus = 0;
+    const int rc = plan_args(M, Mkv, T, H, W, heads, head_dim, dtype, compute_units, &cus, fn);
+    if (rc != RF_OK) return rc;
+    const int64_t N = static_cast<int64_t>(H) * W;
+    rf_attention_split out;
+    memset(&out, 0, sizeof out);
+    out.compute_units = cus;
+    if (dtype == RF_BF16) {
+        const rf::AttnSplit sp = rf::attention_split(static_cast<int64_t>(M) * N, heads, head_dim, N, N * T,
+                                                     Mkv < T ? Mkv : 0, cus);
+        out.tiles = sp.n_tiles;
+        out.whole_tiles = sp.n_direct;
+        out.tail_tiles = sp.n_tail;
+        out.parts = static_cast<int32_t>(sp.split);
+        out.key_tiles_per_part = static_cast<int32_t>(sp.kv_per_split);
+        out.workspace_bytes = sp.ws_bytes;
+    }
+    *plan_out = out;
     return ok();
 }
 

@@ -33,11 +33,12 @@
 //    costs no max reduction. P is rounded to bf16 for the matrix cores and the
 //    row sum adds those same rounded values.
 //  * Workgroup ids are mapped XCD-aware: consecutive ids go round-robin to the
-//    8 XCDs, so tile = (id % 8) * per_xcd + id / 8 gives each XCD a contiguous,
-//    head-major range of tiles and the workgroups resident on one XCD stream
-//    the same head's K/V through that XCD's L2.
+//    device's X XCDs (8 on MI355X), so tile = (id % X) * per_xcd + id / X gives
+//    each XCD a contiguous, head-major range of tiles and the workgroups
+//    resident on one XCD stream the same head's K/V through that XCD's L2.
 //  * Split-key tail (when the caller provides a workspace): one workgroup
-//    fills a CU, so a launch of n tiles runs in ceil(n / 256) rounds and the
+//    fills a CU, so a launch of n tiles runs in ceil(n / CUs) rounds (256 CUs
+//    on MI355X; the count is queried from the device) and the
 //    last round may leave most CUs idle. The tiles beyond the last full round
 //    are then split along the keys into parts that run as extra workgroups;
 //    each part writes its unnormalised (O, m, l) in fp32, and a small kernel
@@ -46,6 +47,8 @@
 //    of frames in key tiles that never cross a frame; masked frames are
 //    never read.
 // The fp32 kernel at the end is a plain correctness path (fp32 throughout).
+#include <atomic>
+
 #include "rf_internal.h"
 
 namespace rf {
@@ -94,11 +97,9 @@ constexpr int kBr = 32 * kWaves;   // query rows per workgroup
 // it takes twice the keys (the registers and LDS that head dimension leaves free
 // hold them).
 __host__ __device__ constexpr int key_tile(int head_dim) { return head_dim == 64 ? RF_ATTN_BC64 : RF_ATTN_BC; }
-constexpr int kXcds = 8;
-// Split-key tail: compute units a round of whole tiles fills (one workgroup
-// per CU on MI355X), the most parts a tail tile is cut into, and the fewest
-// key tiles a part may have.
-constexpr int kSplitCUs = 256;
+// Split-key tail: the most parts a tail tile is cut into and the fewest key
+// tiles a part may have. A round of whole tiles fills the device's compute
+// units (one workgroup per CU), queried at launch.
 constexpr int kMaxSplit = 8;
 constexpr int kMinKvPerSplit = 8;
 constexpr float kRebaseBound = RF_ATTN_REBASE_BOUND;   // largest tile row sum kept without a rebase
@@ -116,7 +117,8 @@ struct AttnKArgs {
     int32_t n_qtiles;
     int32_t total_tiles;    // tiles computed whole (all tiles when there is no split)
     int32_t per_xcd;
-    int32_t grid_direct;    // workgroups of the whole tiles (per_xcd * 8)
+    int32_t xcds;           // XCDs of the device: workgroup id i runs on XCD i % xcds
+    int32_t grid_direct;    // workgroups of the whole tiles (per_xcd * xcds)
     int32_t split;          // parts per tail tile (0: no split)
     int32_t kv_per_split;   // key tiles per part
     float *ws_o;            // [tail tile * split + part][kBr][D] unnormalised O
@@ -313,7 +315,7 @@ void attn_bf16_kernel(const AttnKArgs a) {
     const int bid = blockIdx.x;
     int tile, part = -1;
     if (bid < a.grid_direct) {
-        tile = (bid % kXcds) * a.per_xcd + bid / kXcds;
+        tile = (bid % a.xcds) * a.per_xcd + bid / a.xcds;
         if (tile >= a.total_tiles) return;
     } else {   // a part of a tail tile (tail tiles follow the whole ones in tile order)
         const int u = bid - a.grid_direct;
@@ -715,19 +717,45 @@ __global__ __launch_bounds__(2 * kF32Rows) void attn_f32_kernel(const AttnF32Arg
 
 }  // namespace
 
-AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv) {
+hipError_t device_geometry(DeviceGeometry *out) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int64_t> cached[kMaxDevices];   // (cus << 32 | xcds), 0 until queried
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int64_t v = cached[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int cus = 0, xcds = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        e = hipDeviceGetAttribute(&xcds, hipDeviceAttributeNumberOfXccs, dev);
+        if (e != hipSuccess || xcds < 1) xcds = 1;   // no XCD count reported: one L2 domain
+        if (cus < 1) return hipErrorInvalidDevice;
+        if (xcds > cus) xcds = cus;
+        v = (static_cast<int64_t>(cus) << 32) | static_cast<uint32_t>(xcds);
+        cached[dev].store(v, std::memory_order_relaxed);
+    }
+    out->cus = static_cast<int32_t>(v >> 32);
+    out->xcds = static_cast<int32_t>(v & 0xffffffff);
+    return hipSuccess;
+}
+
+AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv,
+                          int32_t cus) {
     AttnSplit sp{};
     const int64_t total = (Mq + kBr - 1) / kBr * heads;
     const int64_t kBc = key_tile(head_dim);
     const int64_t kv_tiles = n_kv > 0 ? static_cast<int64_t>(n_kv) * ((N + kBc - 1) / kBc) : (S + kBc - 1) / kBc;
-    const int64_t tail = total % kSplitCUs;
+    const int64_t tail = total % cus;
+    sp.n_tiles = total;
     sp.n_direct = total;
     if (tail == 0) return sp;
     // tail time in rounds of whole tiles for s parts: ceil(tail * s / CUs) / s
     int best_s = 1;
     double best = 1.0;
     for (int s = 2; s <= kMaxSplit && kv_tiles / s >= kMinKvPerSplit; ++s) {
-        const double cost = static_cast<double>((tail * s + kSplitCUs - 1) / kSplitCUs) / s;
+        const double cost = static_cast<double>((tail * s + cus - 1) / cus) / s;
         if (cost < best - 1e-9) {
             best = cost;
             best_s = s;
@@ -755,22 +783,25 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         a.Mq = Mq;
         a.heads = p.heads;
         const int64_t nq = (Mq + kBr - 1) / kBr;
+        const int32_t xcds = p.geo.xcds;
+        if (p.geo.cus < 1 || xcds < 1 || xcds > 64) return hipErrorInvalidValue;
         AttnSplit sp{};
         sp.n_direct = nq * p.heads;
         if (p.ws) {
-            sp = attention_split(Mq, p.heads, p.head_dim, p.N, p.S, p.n_kv);
+            sp = attention_split(Mq, p.heads, p.head_dim, p.N, p.S, p.n_kv, p.geo.cus);
             if (sp.split > 0 && p.ws_bytes < sp.ws_bytes) return hipErrorInvalidValue;
         }
         const int64_t total = sp.n_direct;
-        const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-        if (nq * p.heads > 0x7fffffffLL / kXcds) return hipErrorInvalidConfiguration;
+        const int64_t per_xcd = (total + xcds - 1) / xcds;
+        if (nq * p.heads > 0x7fffffffLL / 64) return hipErrorInvalidConfiguration;
         // per-lane load offsets inside a tile are 32-bit: a tile's token rows must span < 2 GiB
         const int64_t kBc = key_tile(p.head_dim);
         if (static_cast<int64_t>(p.heads) * p.head_dim * 2 * kBc >= 0x7fffffffLL) return hipErrorInvalidConfiguration;
         a.n_qtiles = static_cast<int32_t>(nq);
         a.total_tiles = static_cast<int32_t>(total);
         a.per_xcd = static_cast<int32_t>(per_xcd);
-        a.grid_direct = static_cast<int32_t>(per_xcd * kXcds);
+        a.xcds = xcds;
+        a.grid_direct = static_cast<int32_t>(per_xcd * xcds);
         a.split = static_cast<int32_t>(sp.split);
         a.kv_per_split = static_cast<int32_t>(sp.kv_per_split);
         const int64_t n_parts = sp.n_tail * sp.split;
@@ -785,7 +816,7 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         for (int i = 0; i < p.n_kv; ++i) a.kvf[i] = p.kvf[i];
         if (p.n_kv > 0 && static_cast<int64_t>(p.n_kv) * a.tiles_per_frame > 0x7fffffffLL)
             return hipErrorInvalidConfiguration;
-        const dim3 grid(static_cast<uint32_t>(per_xcd * kXcds + n_parts)), block(kThreads);
+        const dim3 grid(static_cast<uint32_t>(per_xcd * xcds + n_parts)), block(kThreads);
         if (p.n_kv > 0) {
             if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
             else hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);

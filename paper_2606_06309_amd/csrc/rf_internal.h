@@ -11,6 +11,15 @@ namespace rf {
 
 constexpr int kMaxFrames = RF_MAX_FRAMES;
 
+// Compute units and XCDs (each with its own L2) of the current device, queried
+// once per device and kept.
+struct DeviceGeometry {
+    int32_t cus;
+    int32_t xcds;
+};
+
+hipError_t device_geometry(DeviceGeometry *out);
+
 // Keyframe-query attention launch description. Frame ids travel by value in
 // the kernel arguments.
 struct AttnParams {
@@ -31,12 +40,15 @@ struct AttnParams {
     // optional workspace for the split-key tail (NULL: no split)
     void *ws;
     int64_t ws_bytes;
+    // the device the launch runs on (bf16: the split plan and the XCD mapping)
+    DeviceGeometry geo;
 };
 
-// How the bf16 attention of Mq query rows is cut: n_direct whole tiles, then
-// n_tail tiles split into `split` parts of kv_per_split key tiles (split = 0:
-// no split), needing ws_bytes of workspace.
+// How the bf16 attention of Mq query rows is cut on a device of `cus` compute
+// units: n_direct whole tiles, then n_tail tiles split into `split` parts of
+// kv_per_split key tiles (split = 0: no split), needing ws_bytes of workspace.
 struct AttnSplit {
+    int64_t n_tiles;
     int64_t n_direct;
     int64_t n_tail;
     int64_t split;
@@ -44,7 +56,9 @@ struct AttnSplit {
     int64_t ws_bytes;
 };
 
-AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv);
+AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv,
+                          int32_t cus);
+
 
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream);
 

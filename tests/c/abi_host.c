@@ -55,10 +55,15 @@ int main(void) {
                cache.after_slot[4], a);
     }
 
-    {   /* workspace of the split-key tail at 33 x 45 x 80, 24 heads */
+    {   /* workspace and plan of the split-key tail at 33 x 45 x 80, 24 heads, on 256 compute units */
         int64_t bytes = 0;
-        if (rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, RF_BF16, &bytes) != RF_OK) return 1;
+        rf_attention_split plan;
+        if (rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, RF_BF16, 256, &bytes) != RF_OK) return 1;
+        if (rf_attention_plan(8, 33, 33, 45, 80, 24, 128, RF_BF16, 256, &plan) != RF_OK) return 1;
         printf("workspace %lld\n", (long long)bytes);
+        printf("plan %lld %lld %lld %d %d %lld %d\n", (long long)plan.tiles, (long long)plan.whole_tiles,
+               (long long)plan.tail_tiles, plan.parts, plan.key_tiles_per_part, (long long)plan.workspace_bytes,
+               plan.compute_units);
     }
 
     /* an error: described, nothing written */

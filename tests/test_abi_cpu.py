@@ -8,6 +8,7 @@ import re
 
 import numpy as np
 import pytest
+import torch
 
 import oracle
 
@@ -168,20 +169,75 @@ def test_frame_attention_validation(kwargs, status):
 
 def test_attention_workspace_sizes():
     # 2,712 tiles of 256 rows at 33 x 45 x 80, 24 heads: 152 beyond 10 rounds, split in 5
-    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16) == 152 * 5 * 256 * (128 * 4 + 8)
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16, 256) == 152 * 5 * 256 * (128 * 4 + 8)
     # 40 heads, 6 keyframes of 45 x 80: 3,400 tiles, 72 beyond 13 rounds, split in 7
-    assert rf.rf_attention_workspace(6, 21, 21, 45, 80, 40, 128, rf.RF_BF16) == 72 * 7 * 256 * 520
+    assert rf.rf_attention_workspace(6, 21, 21, 45, 80, 40, 128, rf.RF_BF16, 256) == 72 * 7 * 256 * 520
     # whole rounds need nothing; fp32 never splits; too few key tiles to split
-    assert rf.rf_attention_workspace(8, 33, 33, 48, 64, 24, 128, rf.RF_BF16) == 0
-    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_F32) == 0
-    assert rf.rf_attention_workspace(3, 5, 5, 8, 8, 2, 64, rf.RF_BF16) == 0
+    assert rf.rf_attention_workspace(8, 33, 33, 48, 64, 24, 128, rf.RF_BF16, 256) == 0
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_F32, 256) == 0
+    assert rf.rf_attention_workspace(3, 5, 5, 8, 8, 2, 64, rf.RF_BF16, 256) == 0
     n = ctypes.c_int64(0)
-    for args, status in [((0, 5, 5, 8, 8, 2, 64, 0), rf.RF_ERR_INVALID_ARG),
-                         ((6, 5, 5, 8, 8, 2, 64, 0), rf.RF_ERR_RANGE),
-                         ((2, 5, 5, 8, 8, 2, 96, 0), rf.RF_ERR_UNSUPPORTED),
-                         ((2, 5, 300, 8, 8, 2, 64, 0), rf.RF_ERR_RANGE)]:
+    for args, status in [((0, 5, 5, 8, 8, 2, 64, 0, 256), rf.RF_ERR_INVALID_ARG),
+                         ((6, 5, 5, 8, 8, 2, 64, 0, 256), rf.RF_ERR_RANGE),
+                         ((2, 5, 5, 8, 8, 2, 96, 0, 256), rf.RF_ERR_UNSUPPORTED),
+                         ((2, 5, 300, 8, 8, 2, 64, 0, 256), rf.RF_ERR_RANGE),
+                         ((2, 5, 5, 8, 8, 2, 64, 0, -1), rf.RF_ERR_RANGE),
+                         ((2, 5, 5, 8, 8, 2, 64, 0, 65537), rf.RF_ERR_RANGE)]:
         assert lib.rf_attention_workspace(*args, ctypes.byref(n)) == status
-    assert lib.rf_attention_workspace(2, 5, 5, 8, 8, 2, 64, 0, None) == rf.RF_ERR_INVALID_ARG
+    assert lib.rf_attention_workspace(2, 5, 5, 8, 8, 2, 64, 0, 256, None) == rf.RF_ERR_INVALID_ARG
+
+
+# The split plan of the long workload (33 frames of 45 x 80, 24 heads x 128, 8
+# keyframes: 28,800 query rows = 113 tiles of 256 per head, 2,712 tiles; 118,800
+# keys = 1,857 tiles of 64) on three device sizes, worked by hand. s parts of
+# each of the t tail tiles take ceil(t * s / CUs) / s rounds (s = 1: one round);
+# the smallest s of the least cost wins, parts need >= 8 key tiles, s <= 8.
+#   256 CUs: t = 2712 - 10 * 256 = 152; s = 2..8 cost 1, 2/3, 3/4, 3/5, 2/3, 5/7, 5/8 -> s = 5, 372 key tiles a part
+#   128 CUs: t = 2712 - 21 * 128 = 24; s = 5 fits 120 parts in one round (1/5); s = 6..8 need two -> s = 5
+#    80 CUs: t = 2712 - 33 * 80 = 72; every s needs s rounds (72 s / 80 > s - 1) -> cost 1, no split
+LONG_PLANS = {
+    256: dict(tiles=2712, whole_tiles=2560, tail_tiles=152, parts=5, key_tiles_per_part=372,
+              workspace_bytes=152 * 5 * 256 * 520, compute_units=256),
+    128: dict(tiles=2712, whole_tiles=2688, tail_tiles=24, parts=5, key_tiles_per_part=372,
+              workspace_bytes=24 * 5 * 256 * 520, compute_units=128),
+    80: dict(tiles=2712, whole_tiles=2712, tail_tiles=0, parts=0, key_tiles_per_part=0,
+             workspace_bytes=0, compute_units=80),
+}
+
+
+@pytest.mark.parametrize("cus", sorted(LONG_PLANS))
+def test_attention_plan_by_compute_units(cus):
+    plan = rf.rf_attention_plan(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16, cus)
+    assert plan == LONG_PLANS[cus]
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16, cus) == plan["workspace_bytes"]
+
+
+def test_attention_plan_head_dim_64_and_fp32():
+    # the CogVideoX-v1.5 shape (11 frames of 48 x 85, 48 heads x 64, 4 keyframes): 16,320 rows =
+    # 64 tiles per head, 3,072 tiles = 12 whole rounds of 256: nothing to split; on 100 CUs
+    # 72 tiles remain, 44,880 keys are 351 tiles of 128: s = 4 puts 288 parts in 3 rounds (3/4)
+    assert rf.rf_attention_plan(4, 11, 11, 48, 85, 48, 64, rf.RF_BF16, 256)["parts"] == 0
+    p = rf.rf_attention_plan(4, 11, 11, 48, 85, 48, 64, rf.RF_BF16, 100)
+    assert (p["tail_tiles"], p["parts"], p["key_tiles_per_part"]) == (72, 4, 88)
+    assert p["workspace_bytes"] == 72 * 4 * 256 * (64 * 4 + 8)
+    f = rf.rf_attention_plan(4, 11, 11, 48, 85, 48, 64, rf.RF_F32, 256)
+    assert f == dict(tiles=0, whole_tiles=0, tail_tiles=0, parts=0, key_tiles_per_part=0,
+                     workspace_bytes=0, compute_units=256)
+
+
+def test_attention_plan_of_the_current_device_needs_one():
+    if _gpu_present():
+        pytest.skip("a device is present")
+    n = ctypes.c_int64(0)
+    assert lib.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16, 0, ctypes.byref(n)) == rf.RF_ERR_HIP
+    assert "cannot query" in lib.rf_last_error().decode()
+
+
+def _gpu_present():
+    try:
+        return torch.cuda.is_available()
+    except Exception:
+        return False
 
 
 def _attn_ws(ws=0x50000000, ws_bytes=1 << 30, T=8, H=16, W=16, heads=2, d=128, ids=(0, 5), out=O_):
@@ -192,13 +248,15 @@ def _attn_ws(ws=0x50000000, ws_bytes=1 << 30, T=8, H=16, W=16, heads=2, d=128, i
 
 @pytest.mark.parametrize("kwargs,status", [
     (dict(ws=0), rf.RF_ERR_INVALID_ARG),
-    (dict(ws_bytes=1000), rf.RF_ERR_INVALID_ARG),
+    (dict(ws_bytes=-1), rf.RF_ERR_INVALID_ARG),
     (dict(ws=0x50000008), rf.RF_ERR_UNSUPPORTED),
     (dict(ws=A + 64), rf.RF_ERR_INVALID_ARG),          # workspace inside q
     (dict(ws=O_ - 64), rf.RF_ERR_INVALID_ARG),         # workspace running into out
 ])
 def test_attention_ws_validation(kwargs, status):
-    assert rf.rf_attention_workspace(2, 8, 8, 16, 16, 2, 128, rf.RF_BF16) > 0
+    # (a workspace smaller than the device's plan needs is checked after the device
+    # query; its GPU test is in tests/test_gpu_limits.py)
+    assert rf.rf_attention_workspace(2, 8, 8, 16, 16, 2, 128, rf.RF_BF16, 256) > 0
     assert _attn_ws(**kwargs) == status
     assert lib.rf_last_error().decode().startswith("rf_keyframe_attention_ws")
 
@@ -291,7 +349,7 @@ def test_sizes_overflowing_byte_counts_are_range_errors():
     assert lib.rf_keyframe_attention(A, B_, A + 4096, B_ + 4096, ids, 2, 4, big, big, 8, 128,
                                      rf.RF_BF16, None) == rf.RF_ERR_RANGE
     n = ctypes.c_int64(0)
-    assert lib.rf_attention_workspace(2, 4, 4, big, big, 8, 128, rf.RF_BF16, ctypes.byref(n)) == rf.RF_ERR_RANGE
+    assert lib.rf_attention_workspace(2, 4, 4, big, big, 8, 128, rf.RF_BF16, 256, ctypes.byref(n)) == rf.RF_ERR_RANGE
     m = (ctypes.c_uint8 * 5)(1, 0, 1, 0, 1)
     ts = (ctypes.c_double * 3)(24.0, 21.0, 23.0)
     assert lib.rf_project_latents(A, B_, ts, m, big, 16, 5, big, 16, rf.RF_F32, None) == rf.RF_ERR_RANGE

@@ -55,12 +55,18 @@ def test_source_digest_ignores_comments_and_whitespace(tmp_path):
     assert bench.source_digest(str(a)) != bench.source_digest(str(c))
 
 
-def test_committed_traffic_matches_the_attention_code():
-    """The committed counter summary was taken on the current attention code, so
-    the bench reports its traffic (and it exceeds the algorithmic bytes)."""
+def test_committed_traffic_is_reported_only_for_the_code_it_was_taken_on():
+    """The bench reports the committed counter summary's traffic only while the
+    attention code has the digest recorded there (then it exceeds the
+    algorithmic bytes); after a change of the code it reports none."""
+    path = os.path.join(ROOT, "profiles", "attn_bf16_long_traffic.txt")
+    recorded = [l.split(":", 1)[1].strip() for l in open(path) if l.startswith("attention code sha256")]
+    current = bench.source_digest(os.path.join(ROOT, "paper_2606_06309_amd", "csrc", "rf_attention.hip"))
     traffic = bench.profiled_traffic("long")
-    assert isinstance(traffic, int)
-    assert traffic > 1813708800
+    if recorded == [current]:
+        assert isinstance(traffic, int) and traffic > 1813708800
+    else:
+        assert traffic is None
 
 
 def test_side_section_failure_is_reported(capsys):

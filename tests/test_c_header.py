@@ -32,7 +32,7 @@ def output(tmp_path_factory):
 
 
 def test_keyframe_sets(output):
-    assert output["abi"] == ["1"]
+    assert output["abi"] == ["2"]
     assert [int(x) for x in output["select"]] == oracle.select_keyframes([12, 4, 4, 20], 21).tolist()
     assert [int(x) for x in output["uniform"]] == oracle.uniform_keyframes(21, 6).tolist()
 
@@ -59,5 +59,8 @@ def test_cache_bookkeeping(output):
 
 def test_workspace_and_error(output):
     assert int(output["workspace"][0]) == 152 * 5 * 256 * (128 * 4 + 8)
+    # 28,800 query rows = 113 tiles of 256 per head, 24 heads = 2,712 tiles = 10 rounds of 256 + 152;
+    # 1,857 key tiles of 64 in 5 parts of 372
+    assert [int(x) for x in output["plan"]] == [2712, 2560, 152, 5, 372, 152 * 5 * 256 * 520, 256]
     err = output["error"]
     assert err[0] == "RF_ERR_RANGE" and err[1] == "n=-7" and err[2].startswith("msg=rf_keyframes_uniform")

@@ -98,3 +98,31 @@ def test_rolling_cache_255_frames():
     assert (np.abs(kf[1:] - exp) <= bound).all()
     assert not kf[0].any()                                   # the keyframe's rows are untouched
     assert np.array_equal(_bits(k)[w.N:], _bits(v)[w.N:])
+
+
+# --- the device's geometry: the split plan follows its compute units ---------------
+
+def test_plan_follows_the_device():
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    plan = rf.rf_attention_plan(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16)
+    assert plan["compute_units"] == cus
+    assert plan == rf.rf_attention_plan(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16, cus)
+    assert plan["whole_tiles"] % cus == 0 or plan["parts"] == 0
+    assert rf.rf_attention_workspace(8, 33, 33, 45, 80, 24, 128, rf.RF_BF16) == plan["workspace_bytes"]
+
+
+def test_too_small_workspace_is_rejected_before_launch():
+    """A workspace smaller than the current device's plan needs is refused
+    (checked after the device query, before anything is launched): the output
+    buffer keeps its sentinel."""
+    w = workloads.custom(8, 16, 16, 2, 128, (0, 5), dtype="bf16", seed=51)
+    need = rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, rf.RF_BF16)
+    assert need > 0
+    q, k, v = workloads.make_qkv(w, device="cuda")
+    out = torch.full((w.M * w.N, w.heads, w.head_dim), 7.0, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(need - 16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(rf.RhymeFlowError) as e:
+        rf.rf_keyframe_attention_ws(q, k, v, w.keyframes, w.T, w.H, w.W, out=out, workspace=ws)
+    assert e.value.status == rf.RF_ERR_INVALID_ARG and "needed" in str(e.value)
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
