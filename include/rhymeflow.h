@@ -196,6 +196,30 @@ int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *
                              int64_t workspace_bytes, void *stream);
 
 /*
+ * rf_keyframe_attention_ws without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc). The split-key tail's partial
+ * results go to a static device array of RF_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends; the call
+ * allocates nothing. Results equal rf_keyframe_attention_ws's bit for bit (the
+ * same plan and kernels).
+ *
+ * Shapes whose split-key tail needs more than RF_NOALLOC_SCRATCH_BYTES on the
+ * current device (rf_attention_workspace with compute_units = 0) are refused
+ * with RF_ERR_RANGE; at 256 compute units that is only the case for
+ * launches past about 200 tail tiles at head_dim 128, none of the paper's
+ * shapes. All calls on one GPU share its array: two calls that overlap in time
+ * on one GPU (different streams or threads) race on it, so serialise them.
+ * The first call on each device looks up the array's device address (a HIP
+ * query); a failure there returns RF_ERR_HIP.
+ * Arguments and other errors as rf_keyframe_attention.
+ */
+#define RF_NOALLOC_SCRATCH_BYTES (160LL << 20)
+int rf_keyframe_attention_noalloc(const void *q, const void *k, const void *v, void *out,
+                                  const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                                  int32_t heads, int32_t head_dim, int32_t dtype, void *stream);
+
+/*
  * Bytes of workspace rf_keyframe_attention_ws (Mkv = T) or rf_frame_attention
  * (Mkv key/value frames) uses for these sizes on a device of compute_units
  * compute units (0 when nothing is split, always 0 for RF_F32). The split-key

@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "librhymeflow.so")
 ARCH = "gfx950"
 
 SOURCES = ["rf_abi.cpp", "rf_attention.hip", "rf_project.hip", "rf_gather.hip", "rf_similarity.hip",
-           "rf_cache.hip", "rf_probe.hip"]
+           "rf_cache.hip", "rf_probe.hip", "rf_noalloc.hip"]
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -31,7 +31,7 @@ EXPORTED = [
     "rf_status_string", "rf_last_error", "rf_abi_version",
     "rf_select_keyframes", "rf_keyframes_stride", "rf_keyframes_uniform",
     "rf_project_latents", "rf_keyframe_attention", "rf_keyframe_attention_ws", "rf_attention_workspace",
-    "rf_attention_plan",
+    "rf_attention_plan", "rf_keyframe_attention_noalloc",
     "rf_frame_attention",
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
@@ -133,6 +133,10 @@ lib.rf_frame_attention.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32p, _i32,
 lib.rf_keyframe_attention_ws.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
                                          _i32, _i32, _i32, _vp, _i64, _vp]
 lib.rf_keyframe_attention_ws.restype = ctypes.c_int
+lib.rf_keyframe_attention_noalloc.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32,
+                                              _i32, _i32, _i32, _vp]
+lib.rf_keyframe_attention_noalloc.restype = ctypes.c_int
+RF_NOALLOC_SCRATCH_BYTES = 160 << 20
 lib.rf_attention_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64)]
 lib.rf_attention_workspace.restype = ctypes.c_int
 lib.rf_attention_plan.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
@@ -383,6 +387,28 @@ def rf_keyframe_attention_ws(q, k, v, keyframe_ids, T: int, H: int, W: int, out=
     workspace, wbytes = _workspace(workspace, need, q.device, stream)
     _check(lib.rf_keyframe_attention_ws(*ptrs, ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
                                         _dev(workspace, "workspace"), wbytes, _stream(stream)))
+    return out
+
+
+def rf_keyframe_attention_noalloc(q, k, v, keyframe_ids, T: int, H: int, W: int, out=None, stream=None):
+    """rf_keyframe_attention with the split-key tail in the library's static
+    device scratch (no workspace; the library allocates nothing). Calls that
+    overlap in time on one GPU race on that scratch."""
+    if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share a dtype")
+    S, heads, d = q.shape
+    if S != T * H * W:
+        raise ValueError(f"S = {S} differs from T*H*W = {T * H * W}")
+    ids, ids_p = _ids(keyframe_ids)
+    M = ids.size
+    if out is None:
+        out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
+    if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
+        raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
+    _check(lib.rf_keyframe_attention_noalloc(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                             ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype), _stream(stream)))
     return out
 
 

@@ -214,10 +214,12 @@ static int query_geometry(rf::DeviceGeometry *geo, const char *fn) {
     return RF_OK;
 }
 
+// use_scratch: the split tail takes the library's static scratch (the
+// allocation-free entry point) instead of a caller workspace.
 static int attention_call(const void *q, const void *k, const void *v, void *out, const int32_t *q_ids,
                           int32_t M, const int32_t *kv_ids, int32_t Mkv, int32_t T, int32_t H, int32_t W,
                           int32_t heads, int32_t head_dim, int32_t dtype, void *ws, int64_t ws_bytes,
-                          void *stream, const char *fn) {
+                          void *stream, const char *fn, bool use_scratch = false) {
     if (!q || !k || !v || !out) return fail(RF_ERR_INVALID_ARG, "%s: NULL tensor", fn);
     if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
@@ -262,7 +264,21 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
         rc = query_geometry(&p.geo, fn);
         if (rc != RF_OK) return rc;
     }
-    if (ws) {
+    if (use_scratch) {
+        const int64_t need = attention_ws_need(M, n_kv, T, N, heads, head_dim, dtype, p.geo.cus);
+        if (need > rf::kAttentionScratchBytes)
+            return fail(RF_ERR_RANGE,
+                        "%s: the split-key tail needs %lld bytes of scratch on %d compute units, the static "
+                        "scratch holds %lld (rf_keyframe_attention_ws takes a workspace of any size)",
+                        fn, static_cast<long long>(need), p.geo.cus,
+                        static_cast<long long>(rf::kAttentionScratchBytes));
+        if (need > 0) {
+            const hipError_t e = rf::attention_scratch(&p.ws);
+            if (e != hipSuccess)
+                return fail(RF_ERR_HIP, "%s: cannot look up the static scratch: %s", fn, hipGetErrorString(e));
+            p.ws_bytes = rf::kAttentionScratchBytes;
+        }
+    } else if (ws) {
         const int64_t need = attention_ws_need(M, n_kv, T, N, heads, head_dim, dtype, p.geo.cus);
         if (ws_bytes < need)
             return fail(RF_ERR_INVALID_ARG, "%s: workspace of %lld bytes, %lld needed on %d compute units", fn,
@@ -303,6 +319,13 @@ int rf_keyframe_attention_ws(const void *q, const void *k, const void *v, void *
     if (!workspace) return fail(RF_ERR_INVALID_ARG, "%s: NULL workspace", fn);
     return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype,
                           workspace, workspace_bytes, stream, fn);
+}
+
+int rf_keyframe_attention_noalloc(const void *q, const void *k, const void *v, void *out,
+                                  const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                                  int32_t heads, int32_t head_dim, int32_t dtype, void *stream) {
+    return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype, nullptr, 0,
+                          stream, "rf_keyframe_attention_noalloc", true);
 }
 
 int rf_frame_attention(const void *q, const void *k, const void *v, void *out,

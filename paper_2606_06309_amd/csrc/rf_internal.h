@@ -62,6 +62,12 @@ AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N
 
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream);
 
+// Static split-tail scratch of the allocation-free attention entry point (a
+// file-scope device array in rf_noalloc.hip): its size, and its device address
+// on the current device (looked up once per device).
+constexpr int64_t kAttentionScratchBytes = int64_t(160) << 20;
+hipError_t attention_scratch(void **out);
+
 struct ProjParams {
     const void *latents;
     void *out;
