@@ -13,12 +13,17 @@ for the speedup.
 
 Prints ONE JSON line. `value` is keyframe-query attention TFLOP per second of
 whole-step time; `roofline` describes the attention kernel alone, timed with
-HIP events around each launch on the stream it runs on. Side sections time the
-bandwidth kernels (projection, gather, scatter), content-aware selection
-(frame similarity and Alg. 1's scan), the rolling cache of App. B.2
+HIP events around each launch on the stream it runs on, with the shader clock
+sampled under that load. Side sections time the bandwidth kernels
+(projection, gather, scatter), content-aware selection (frame similarity, one
+video and an HBM-sized batch, and Alg. 1's scan), the rolling cache of App. B.2
 (projection of cached states into K and V, shift-and-store), keyframe-only
-attention (a frame-level key/value mask) and a whole denoising schedule of
-Alg. 2 (attention path only) against its dense counterpart.
+attention (a frame-level key/value mask), a whole denoising schedule of Alg. 2
+(attention path only; latent projection, rolling cache with clamped and with
+interpolating labels) against its dense counterpart, the other workloads
+(keyframe-query and all-frame attention at the paper's two model shapes and
+the smaller configurations), and the oracle per configuration beside the
+headline CPU baseline.
 """
 import argparse
 import json
@@ -52,6 +57,8 @@ def parse():
     ap.add_argument("--no-frame-mask", action="store_true")
     ap.add_argument("--no-shard", action="store_true")
     ap.add_argument("--no-peaks", action="store_true")
+    ap.add_argument("--no-configs", action="store_true")
+    ap.add_argument("--no-clock", action="store_true")
     ap.add_argument("--schedule", default="50,8,25,2,3",
                     help="T,T_w,T_mid,n_small,n_large of the multi-step schedule loop")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -282,14 +289,189 @@ def main():
     if not args.no_shard:
         result["head_shard"] = _side("head_shard", head_shard, w, args)
 
+    if not args.no_clock:
+        result["clock"] = _side("clock", clock_sample, lambda: rf.rf_keyframe_attention_ws(
+            q, k, v, w.keyframes, w.T, w.H, w.W, out=attn_out, workspace=ws))
+        if isinstance(result["clock"], dict) and "sclk_mhz" in result["clock"]:
+            # the clock this attention load holds (the 2.5 PFLOP/s peak assumes 2.4 GHz)
+            result["roofline"]["sclk_mhz"] = result["clock"]["sclk_mhz"]
+
+    if not args.no_configs:
+        result["configs"] = _side("configs", other_configs, w.name, args)
+
     if not args.no_peaks:
         result["measured_peaks"] = _side("measured_peaks", measured_peaks, attn_tflops)
 
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = _side("cpu_baseline", cpu_baseline, w, q, k, v, args.cpu_seconds)
+        if isinstance(result["cpu_baseline"], dict) and "error" not in result["cpu_baseline"]:
+            gpu = {name: c.get("keyframe_query", {}).get("tflops") for name, c in
+                   (result.get("configs") or {}).items() if isinstance(c, dict)}
+            gpu[w.name] = attn_tflops
+            result["cpu_baseline"]["per_config"] = _side("cpu_per_config", cpu_per_config, gpu)
 
     print(json.dumps(result), flush=True)
+
+
+def clock_sample(launch, seconds=1.2):
+    """The shader clock while the timed launch runs back to back: one
+    `rocm-smi --showclocks` sample taken in a thread ~0.4 s into a loop of
+    launches that lasts `seconds` (the power-limited clock of this load)."""
+    import re
+    import subprocess
+    import threading
+    import torch
+
+    found = {}
+
+    def sample():
+        time.sleep(0.4)
+        try:
+            out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                                 timeout=20).stdout
+        except (OSError, subprocess.SubprocessError) as e:
+            found["error"] = repr(e)[:200]
+            return
+        for line in out.splitlines():
+            m = re.search(r"\b(sclk|mclk)\b.*?\((\d+)\s*Mhz\)", line, re.I)
+            if m:
+                found.setdefault(m.group(1).lower() + "_mhz", int(m.group(2)))
+
+    th = threading.Thread(target=sample)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    th.start()
+    n = 0
+    while time.perf_counter() - t0 < seconds or th.is_alive():
+        launch()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    th.join()
+    found["launches"] = n
+    found["source"] = "rocm-smi --showclocks, sampled during back-to-back launches of the timed attention call"
+    if "sclk_mhz" in found:
+        print(f"[bench] clock under the attention load: sclk {found['sclk_mhz']} MHz", file=sys.stderr, flush=True)
+    return found
+
+
+OTHER_CONFIGS = ["small", "480p", "720p", "wan-1.3b", "cogvideox"]
+
+
+def other_configs(headline, args):
+    """Keyframe-query attention (with the split-key tail) and the all-frame
+    comparator at the other workloads: the paper's model shapes and the
+    smaller configurations, each warmed for >= 0.3 s before timing."""
+    import torch
+    from paper_2606_06309_amd import accounting, binding as rf, workloads
+
+    res = {}
+    for name in OTHER_CONFIGS:
+        if name == headline:
+            continue
+        w = workloads.WORKLOADS[name]
+        q, k, v = workloads.make_qkv(w, device="cuda")
+        ws = torch.empty(max(16, rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype),
+                             rf.rf_attention_workspace(w.T, w.T, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype)),
+                         dtype=torch.uint8, device="cuda")
+        row = {"shape": [w.T, w.H, w.W], "heads": w.heads, "head_dim": w.head_dim, "keyframes": list(w.keyframes)}
+        for what, ids in (("keyframe_query", list(w.keyframes)), ("all_frame", list(range(w.T)))):
+            out = torch.empty((len(ids) * w.N, w.heads, w.head_dim), dtype=q.dtype, device="cuda")
+
+            def call():
+                rf.rf_keyframe_attention_ws(q, k, v, ids, w.T, w.H, w.W, out=out, workspace=ws)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < 0.3:
+                call()
+                torch.cuda.synchronize()
+            n = max(3, min(20, int(0.4 / max(1e-4, (time.perf_counter() - t0) / 10))))
+            ev = _events(n)
+            for a, b in ev:
+                a.record()
+                call()
+                b.record()
+            torch.cuda.synchronize()
+            ms = _avg_ms(ev)
+            flop = accounting.attention_flops(len(ids) * w.N, w.S, w.head_dim, w.heads)
+            tf = flop / (ms * 1e-3) / 1e12
+            row[what] = {"avg_ms": round(ms, 4), "tflops": round(tf, 2), "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                         "launches": n, "flop_per_launch": flop}
+            del out
+        row["speedup_vs_all_frame"] = round(row["all_frame"]["avg_ms"] / row["keyframe_query"]["avg_ms"], 4)
+        row["ideal_speedup"] = round(accounting.ideal_speedup(w.T, w.M), 4)
+        print(f"[bench] {name}: keyframe-query {row['keyframe_query']['avg_ms']:.3f} ms = "
+              f"{row['keyframe_query']['tflops']:.1f} TFLOP/s, all-frame {row['all_frame']['avg_ms']:.3f} ms, speedup "
+              f"{row['speedup_vs_all_frame']:.3f} (ideal {row['ideal_speedup']:.3f})", file=sys.stderr, flush=True)
+        res[name] = row
+        del q, k, v, ws
+        torch.cuda.empty_cache()
+    return res
+
+
+def cpu_per_config(gpu_tflops):
+    """The oracle per configuration, as the CPU baseline plan states it: the tiny
+    workload in full; the small workload one head in full (all 7,800 rows over
+    20,280 keys) extrapolated to its 12 heads; the larger ones on seeded row
+    samples extrapolated to every (row, head) pair (each costs exactly 4*S*d
+    FLOP); the projection oracle on the 480p latents and the selection oracle
+    (frame cosine on the long workload's latent grid plus Alg. 1's scan) in full."""
+    import numpy as np
+    import oracle
+    from paper_2606_06309_amd import accounting, workloads
+
+    out = {}
+    rng = np.random.default_rng(2027)
+    plan = {"tiny": None, "small": "one head", "480p": 64, "720p": 64, "long": 64, "wan-1.3b": 32, "cogvideox": 16}
+    for name, how in plan.items():
+        w = workloads.WORKLOADS[name]
+        q, k, v = workloads.make_qkv(w)
+        rowmap = oracle.rowmap(w.keyframes, w.N)
+        if how is None:
+            toks, heads = np.repeat(rowmap, w.heads), np.tile(np.arange(w.heads), rowmap.size)
+            label = "in full"
+        elif how == "one head":
+            toks, heads = rowmap, np.zeros(rowmap.size, dtype=np.int64)
+            label = f"head 0 in full ({rowmap.size} rows), extrapolated to {w.heads} heads"
+        else:
+            rows = np.concatenate([rng.choice(rowmap.size, how, replace=False) for _ in range(w.heads)])
+            toks, heads = rowmap[rows], np.repeat(np.arange(w.heads), how)
+            label = f"{how} random rows per head ({toks.size} pairs), extrapolated to {rowmap.size * w.heads} pairs"
+        t0 = time.perf_counter()
+        oracle.attention_pairs(q, k, v, toks, heads)
+        dt = time.perf_counter() - t0
+        pairs_total = rowmap.size * w.heads
+        sec = dt * pairs_total / toks.size
+        flop = accounting.attention_flops(w.M * w.N, w.S, w.head_dim, w.heads)
+        tf = flop / sec / 1e12
+        row = {"seconds": round(sec, 3), "tflops": round(tf, 6), "measured_s": round(dt, 2), "sample": label,
+               "extrapolated": how is not None}
+        g = gpu_tflops.get(name)
+        if g:
+            row["gpu_over_cpu"] = round(g / tf, 1)
+        out[name] = row
+        print(f"[bench] oracle {name}: {sec:.2f} s per launch ({label})", file=sys.stderr, flush=True)
+    w = workloads.WORKLOADS["480p"]
+    Hl, Wl = w.latent_hw
+    lat = workloads.make_latents(w, B=1)
+    mask = oracle.keyframe_mask(w.keyframes, w.T)
+    t0 = time.perf_counter()
+    oracle.project_latents(lat, 1, w.latent_c, w.T, Hl, Wl, w.timesteps, mask)
+    dt = time.perf_counter() - t0
+    nb = accounting.projection_bytes(1, w.latent_c, w.T, Hl * Wl, w.M, 4)
+    out["projection_480p"] = {"seconds": round(dt, 4), "gbs": round(nb / dt / 1e9, 3), "bytes": nb, "sample": "in full"}
+    w = workloads.WORKLOADS["long"]
+    Hl, Wl = w.latent_hw
+    x = workloads.make_scene_latents(1, w.latent_c, w.T, Hl, Wl, tuple(range(5, w.T, 6)), noise=0.5)
+    t0 = time.perf_counter()
+    sim = oracle.frame_cosine(x, 1, w.latent_c, w.T, Hl, Wl)
+    oracle.select_keyframes_adaptive(sim[0], 0.5, w.M, 0.05, 2.0, 2.0)
+    dt = time.perf_counter() - t0
+    out["selection_long"] = {"seconds": round(dt, 4), "gbs": round(x.numel() * 4 / dt / 1e9, 3),
+                             "sample": "in full (frame cosine of f32 proxies + Alg. 1's scan)"}
+    return out
 
 
 def selection(w, args):
@@ -323,10 +505,35 @@ def selection(w, args):
     scan_us = (time.perf_counter() - t0) * 1e6
     nbytes = x.numel() * x.element_size()
     gbs = nbytes / (ms * 1e-3) / 1e9
-    print(f"[bench] selection: similarity {ms * 1e3:.1f} us ({gbs:.0f} GB/s), scan {scan_us:.0f} us, "
+    # the HBM rate: a batch of videos of >= 1 GiB per launch, rotating through 3 such
+    # batches so that no launch finds its input in the 256 MB Infinity Cache
+    per = nbytes
+    B = max(1, -(-(1 << 30) // per))
+    batches = [workloads.make_scene_latents(B, w.latent_c, w.T, Hl, Wl, cuts, noise=0.5, seed=60 + i, device="cuda")
+               for i in range(3)]
+    wsb = torch.empty(rf.rf_frame_similarity_workspace(B, w.latent_c, w.T, Hl, Wl), dtype=torch.uint8, device="cuda")
+    simb = torch.empty((B, w.T, w.T), dtype=torch.float64, device="cuda")
+    for xb in batches:
+        rf.rf_frame_similarity(xb, out=simb, workspace=wsb)
+    torch.cuda.synchronize()
+    evb = _events(6)
+    for i, (a, b) in enumerate(evb):
+        a.record()
+        rf.rf_frame_similarity(batches[i % 3], out=simb, workspace=wsb)
+        b.record()
+    torch.cuda.synchronize()
+    msb = _avg_ms(evb)
+    gbs_b = per * B / (msb * 1e-3) / 1e9
+    del batches, wsb, simb
+    print(f"[bench] selection: similarity {ms * 1e3:.1f} us for one video (cache-resident, {gbs:.0f} GB/s); "
+          f"batched {B} videos {msb * 1e3:.0f} us = {gbs_b:.0f} GB/s from HBM; scan {scan_us:.0f} us, "
           f"keyframes {ids.tolist()}", file=sys.stderr, flush=True)
-    return {"similarity_avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
-            "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "scan_us": round(scan_us, 1),
+    return {"similarity_single": {"avg_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
+                                  "note": "one video re-read each launch: resident in the 256 MB Infinity Cache, "
+                                          "a latency figure, not an HBM rate"},
+            "similarity_batched": {"avg_us": round(msb * 1e3, 2), "bytes": per * B, "batch": B, "rotation_sets": 3,
+                                   "gbs": round(gbs_b, 1), "frac_hbm": round(gbs_b / PEAK_HBM_GBS, 4)},
+            "scan_us": round(scan_us, 1),
             "keyframes": ids.tolist(), "proxies": f"f32 [1][{w.latent_c}][{w.T}][{Hl}][{Wl}], scene cuts {list(cuts)}"}
 
 
@@ -475,6 +682,11 @@ def schedule_loop(w, ws, args):
         and values from the per-layer rolling cache (App. B.2): initialised
         from the last warm-up step's output, shift-and-store at each Rhythmic
         Point, projection into K and V before each keyframe-query attention;
+        each stored state is labelled with its own step, so the skipped steps
+        that follow clamp the weight to 1;
+      cache_interp: as cache, with each stored state labelled with the time its
+        update leads the non-keyframes to, so the skipped steps interpolate
+        (0 < alpha < 1) between the two cached states;
       dense: every step all-frame attention (the reference).
     Q/K/V alternate between two seeded sets. `ideal_flop_ratio` is the FLOP
     ratio of the plan."""
@@ -504,16 +716,18 @@ def schedule_loop(w, ws, args):
             q, k, v = sets[i % 2]
             if mode == "dense" or step["phase"] != "skip":
                 rf.rf_keyframe_attention_ws(q, k, v, all_ids, w.T, w.H, w.W, out=full_out, workspace=ws)
-                if mode == "cache" and nonkey:
+                if mode.startswith("cache") and nonkey:
+                    label = float(step["nonkey_to"] if mode == "cache_interp" else step["t"])
                     if cache is None:
                         if step["phase"] == "warmup" and i + 1 < len(plan) and plan[i + 1]["phase"] == "warmup":
                             continue
-                        cache = rf.rf_cache_init(nonkey, w.T, w.N, D, dt, float(step["t"]), store=store,
-                                                 h_full=full_out)
+                        cache = rf.rf_cache_init(nonkey, w.T, w.N, D, dt, label, store=store, h_full=full_out)
                     elif step["phase"] == "rhythmic":
-                        rf.rf_cache_shift_store(cache, float(step["t"]), store=store, h_full=full_out)
+                        rf.rf_cache_shift_store(cache, label, store=store, h_full=full_out)
             else:
-                if mode == "cache" and cache is not None:
+                if mode.startswith("cache") and cache is not None:
+                    if mode == "cache_interp":
+                        alphas.append(rf.rf_cache_alpha(cache, nonkey[0], float(step["t"])))
                     rf.rf_cache_project_kv(cache, store, k, v, float(step["t"]))
                 else:
                     rf.rf_project_latents(lat, (step["t_start"], step["t_end"], step["t"]), mask, out=proj)
@@ -521,7 +735,8 @@ def schedule_loop(w, ws, args):
                 rf.rf_scatter_frames(kq_out, full_out, ids, w.T, w.N)
 
     times = {}
-    for mode in ("latent", "cache", "dense"):
+    alphas = []
+    for mode in ("latent", "cache", "cache_interp", "dense"):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         a.record()
@@ -534,9 +749,12 @@ def schedule_loop(w, ws, args):
     del sets, lat, proj, kq_out, full_out, store
     return {"T_steps": T_steps, "T_w": T_w, "T_mid": T_mid, "n_small": n_s, "n_large": n_l,
             "steps": led["steps"], "async_ms": round(times["latent"], 2),
-            "async_cache_ms": round(times["cache"], 2), "dense_ms": round(times["dense"], 2),
+            "async_cache_ms": round(times["cache"], 2), "async_cache_interp_ms": round(times["cache_interp"], 2),
+            "cache_interp_alpha_range": [round(min(alphas), 4), round(max(alphas), 4)] if alphas else None,
+            "dense_ms": round(times["dense"], 2),
             "speedup": round(times["dense"] / times["latent"], 4),
             "speedup_cache": round(times["dense"] / times["cache"], 4),
+            "speedup_cache_interp": round(times["dense"] / times["cache_interp"], 4),
             "ideal_flop_ratio": round(led["ratio"], 4),
             "tflops_async": round(led["flop"] / (times["latent"] * 1e-3) / 1e12, 1)}
 
