@@ -803,8 +803,44 @@ def rolling_cache(w, args):
     print(f"[bench] rolling cache: projection {p_ms * 1e3:.1f} us ({p_gbs:.0f} GB/s), "
           f"shift-and-store {s_ms * 1e3:.1f} us ({s_gbs:.0f} GB/s), {len(nk)} frames",
           file=sys.stderr, flush=True)
-    del store, h0, h1, k, v
+
+    # a whole skipped step, unfused (projection into K and V, then attention) against
+    # the fused form (projected tiles formed inside the attention kernel), same inputs
+    q, kq, vq = workloads.make_qkv(w, device="cuda")
+    ids = list(w.keyframes)
+    out = torch.empty((w.M * w.N, w.heads, w.head_dim), dtype=q.dtype, device="cuda")
+    wsa = torch.empty(max(16, rf.rf_attention_workspace(w.M, w.T, w.T, w.H, w.W, w.heads, w.head_dim, q.dtype)),
+                      dtype=torch.uint8, device="cuda")
+    t_skip = t + 1.0
+
+    def unfused():
+        rf.rf_cache_project_kv(c, store, kq, vq, t_skip)
+        rf.rf_keyframe_attention_ws(q, kq, vq, ids, w.T, w.H, w.W, out=out, workspace=wsa)
+
+    def fused():
+        rf.rf_keyframe_attention_cached(q, kq, vq, ids, w.T, w.H, w.W, c, store, t_skip, out=out, workspace=wsa)
+
+    step = {}
+    for name, fn in (("unfused", unfused), ("fused", fused)) * 2:    # interleaved twice, best kept
+        fn()
+        torch.cuda.synchronize()
+        n_s = max(3, min(args.steps, 6))
+        ev = _events(n_s)
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        step[name] = min(step.get(name, 1e30), _avg_ms(ev))
+    flop = accounting.attention_flops(w.M * w.N, w.S, w.head_dim, w.heads)
+    print(f"[bench] skipped step with the rolling cache: unfused {step['unfused']:.3f} ms, "
+          f"fused {step['fused']:.3f} ms", file=sys.stderr, flush=True)
+    del store, h0, h1, k, v, q, kq, vq, out, wsa
     return {"cached_frames": len(nk), "frame_bytes": fb,
+            "skip_step": {"unfused_ms": round(step["unfused"], 4), "fused_ms": round(step["fused"], 4),
+                          "unfused_tflops": round(flop / (step["unfused"] * 1e-3) / 1e12, 2),
+                          "fused_tflops": round(flop / (step["fused"] * 1e-3) / 1e12, 2),
+                          "fused_over_unfused": round(step["unfused"] / step["fused"], 4)},
             "projection": {"bytes": pb, "avg_us": round(p_ms * 1e3, 2), "gbs": round(p_gbs, 1),
                            "frac_hbm": round(p_gbs / PEAK_HBM_GBS, 4)},
             "shift_store": {"bytes": sb, "avg_us": round(s_ms * 1e3, 2), "gbs": round(s_gbs, 1),

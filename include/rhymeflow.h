@@ -483,6 +483,37 @@ int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *
                         const int32_t *frames, int32_t n, double t_skip, void *stream);
 
 /*
+ * Keyframe-query attention at a skipped step with the cached frames' projected
+ * states as their keys and values, formed inside the attention kernel (App. B.2,
+ * attention computation at skipped steps: every cached non-keyframe's key and
+ * value are h = (1 - alpha) h_before + alpha h_after, alpha as in
+ * rf_cache_alpha at t_skip). The result equals rf_cache_project_kv(cache, store,
+ * k, v, NULL, 0, t_skip) followed by rf_keyframe_attention_ws on the modified k
+ * and v, up to fp32 summation order, but k and v are neither written nor read
+ * for cached frames: a key tile of a cached frame loads the frame's two cached
+ * states and forms the projected tile in LDS (fp32 fmaf(alpha, h_after,
+ * (1 - alpha) h_before), rounded once to bf16, as rf_cache_project_kv does). The
+ * key loop walks frames in frame-aligned tiles (a frame's last tile partial when
+ * N is not a multiple of the key tile).
+ *
+ * cache: initialised (rf_cache_init) for T frames of H*W rows of heads*head_dim
+ *   elements in bf16; every cached frame is projected, the others take k and v.
+ * store: the cache's device store (rf_cache_store_bytes bytes), 16-byte
+ *   aligned, not overlapping out.
+ * workspace / workspace_bytes: as rf_keyframe_attention_ws (the same plan and
+ *   size, rf_attention_workspace with Mkv = T).
+ * dtype: RF_BF16 only (RF_ERR_UNSUPPORTED otherwise).
+ * Other arguments and errors as rf_keyframe_attention_ws; RF_ERR_INVALID_ARG
+ * also for a cache that is not initialised, inconsistent, or of another shape
+ * or dtype, a NULL store and a non-finite t_skip.
+ */
+int rf_keyframe_attention_cached(const void *q, const void *k, const void *v, void *out,
+                                 const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                                 int32_t heads, int32_t head_dim, int32_t dtype, const rf_rolling_cache *cache,
+                                 const void *store, double t_skip, void *workspace, int64_t workspace_bytes,
+                                 void *stream);
+
+/*
  * Progressive asynchronous schedule (Eq. 2; Alg. 2), host only.
  *
  * For the denoising steps t = T down to 1: the first T_w steps (t > T - T_w)

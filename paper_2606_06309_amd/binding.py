@@ -36,7 +36,7 @@ EXPORTED = [
     "rf_gather_frames", "rf_scatter_frames",
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
-    "rf_cache_project_kv", "rf_async_schedule",
+    "rf_cache_project_kv", "rf_keyframe_attention_cached", "rf_async_schedule",
     "rf_probe_mfma_bf16", "rf_probe_hbm_read",
 ]
 
@@ -167,6 +167,9 @@ lib.rf_cache_alpha.argtypes = [_cachep, _i32, ctypes.c_double, _dp]
 lib.rf_cache_alpha.restype = ctypes.c_int
 lib.rf_cache_project_kv.argtypes = [_cachep, _vp, _vp, _vp, _i32p, _i32, ctypes.c_double, _vp]
 lib.rf_cache_project_kv.restype = ctypes.c_int
+lib.rf_keyframe_attention_cached.argtypes = [_vp, _vp, _vp, _vp, _i32p, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                             _cachep, _vp, ctypes.c_double, _vp, _i64, _vp]
+lib.rf_keyframe_attention_cached.restype = ctypes.c_int
 lib.rf_async_schedule.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(rf_step_plan), _i32p, _i32p]
 lib.rf_async_schedule.restype = ctypes.c_int
 lib.rf_probe_mfma_bf16.argtypes = [_vp, _i32, _i32, _vp, _vp]
@@ -591,6 +594,36 @@ def rf_cache_project_kv(cache: rf_rolling_cache, store: torch.Tensor, k: torch.T
     _check(lib.rf_cache_project_kv(ctypes.byref(cache), _dev(store, "store"), _dev(k, "k"),
                                    _dev(v, "v"), ids_p, n, float(t_skip), _stream(stream)))
     return k, v
+
+
+def rf_keyframe_attention_cached(q, k, v, keyframe_ids, T: int, H: int, W: int, cache: rf_rolling_cache,
+                                 store: torch.Tensor, t_skip: float, out=None, workspace=None, stream=None):
+    """Keyframe-query attention at a skipped step whose cached frames take their
+    projected hidden states (App. B.2) as keys and values, formed inside the
+    kernel; k and v rows of cached frames are not read. The workspace (a device
+    tensor) is allocated here if not given."""
+    if q.dim() != 3 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share one [S][heads][head_dim] shape")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share a dtype")
+    S, heads, d = q.shape
+    if S != T * H * W:
+        raise ValueError(f"S = {S} differs from T*H*W = {T * H * W}")
+    _check_store(store, 2 * cache.n_cached * cache.frame_bytes)
+    ids, ids_p = _ids(keyframe_ids)
+    M = ids.size
+    if out is None:
+        out = _empty((M * H * W, heads, d), q.dtype, q.device, stream)
+    if out.dtype != q.dtype or out.numel() != M * H * W * heads * d:
+        raise ValueError("out must be [M*H*W][heads][head_dim] of q's dtype")
+    ptrs = [_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out")]
+    sp = _dev(store, "store")
+    need = rf_attention_workspace(M, T, T, H, W, heads, d, q.dtype) if M > 0 and workspace is None else 0
+    workspace, wbytes = _workspace(workspace, need, q.device, stream)
+    _check(lib.rf_keyframe_attention_cached(*ptrs, ids_p, M, T, H, W, heads, d, _dtype_code(q.dtype),
+                                            ctypes.byref(cache), sp, float(t_skip), _dev(workspace, "workspace"),
+                                            wbytes, _stream(stream)))
+    return out
 
 
 # --- asynchronous schedule (Eq. 2, Alg. 2) ----------------------------------------

@@ -214,12 +214,23 @@ static int query_geometry(rf::DeviceGeometry *geo, const char *fn) {
     return RF_OK;
 }
 
+// The cache form of an attention call: the cached frames' projected states at
+// t_skip replace their keys and values (already validated).
+struct CacheForm {
+    const rf_rolling_cache *cache;
+    const void *store;
+    double t_skip;
+};
+
+static double cache_alpha(const rf_rolling_cache &c, int32_t f, double t_skip);
+
 // use_scratch: the split tail takes the library's static scratch (the
 // allocation-free entry point) instead of a caller workspace.
 static int attention_call(const void *q, const void *k, const void *v, void *out, const int32_t *q_ids,
                           int32_t M, const int32_t *kv_ids, int32_t Mkv, int32_t T, int32_t H, int32_t W,
                           int32_t heads, int32_t head_dim, int32_t dtype, void *ws, int64_t ws_bytes,
-                          void *stream, const char *fn, bool use_scratch = false) {
+                          void *stream, const char *fn, bool use_scratch = false,
+                          const CacheForm *cf = nullptr) {
     if (!q || !k || !v || !out) return fail(RF_ERR_INVALID_ARG, "%s: NULL tensor", fn);
     if (H <= 0 || W <= 0 || heads <= 0 || head_dim <= 0)
         return fail(RF_ERR_INVALID_ARG, "%s: sizes must be positive (H=%d W=%d heads=%d head_dim=%d)",
@@ -251,6 +262,22 @@ static int attention_call(const void *q, const void *k, const void *v, void *out
         overlaps(out, out_bytes, v, in_bytes))
         return fail(RF_ERR_INVALID_ARG, "%s: out overlaps q, k or v", fn);
     const int32_t n_kv = (kv_ids && Mkv < T) ? Mkv : 0;
+    if (cf) {
+        const rf_rolling_cache &c = *cf->cache;
+        const int64_t store_bytes = 2 * static_cast<int64_t>(c.n_cached) * c.frame_bytes;
+        if (overlaps(out, out_bytes, cf->store, store_bytes))
+            return fail(RF_ERR_INVALID_ARG, "%s: out overlaps the cache store", fn);
+        p.cache_form = 1;
+        p.store = cf->store;
+        for (int32_t f = 0; f < T; ++f) {
+            p.cslot[f] = -1;
+            p.calpha[f] = 0.0f;
+            if (c.after_slot[f] >= 0) {
+                p.cslot[f] = static_cast<int32_t>(c.before_slot[f]) | (static_cast<int32_t>(c.after_slot[f]) << 16);
+                p.calpha[f] = static_cast<float>(cache_alpha(c, f, cf->t_skip));
+            }
+        }
+    }
     if (ws) {
         if (ws_bytes < 0) return fail(RF_ERR_INVALID_ARG, "%s: workspace_bytes < 0", fn);
         if (!aligned16(ws)) return fail(RF_ERR_UNSUPPORTED, "%s: workspace must be 16-byte aligned", fn);
@@ -747,6 +774,33 @@ int rf_cache_project_kv(const rf_rolling_cache *cache, const void *store, void *
         p.alpha[i] = static_cast<float>(cache_alpha(*cache, f, t_skip));
     }
     return launched(rf::launch_cache_projection(p, static_cast<hipStream_t>(stream)), fn);
+}
+
+int rf_keyframe_attention_cached(const void *q, const void *k, const void *v, void *out,
+                                 const int32_t *keyframe_ids, int32_t M, int32_t T, int32_t H, int32_t W,
+                                 int32_t heads, int32_t head_dim, int32_t dtype, const rf_rolling_cache *cache,
+                                 const void *store, double t_skip, void *workspace, int64_t workspace_bytes,
+                                 void *stream) {
+    const char *fn = "rf_keyframe_attention_cached";
+    int rc = check_cache(cache, fn);
+    if (rc != RF_OK) return rc;
+    if (!store) return fail(RF_ERR_INVALID_ARG, "%s: NULL store", fn);
+    if (!aligned16(store)) return fail(RF_ERR_UNSUPPORTED, "%s: store must be 16-byte aligned", fn);
+    if (!isfinite(t_skip)) return fail(RF_ERR_INVALID_ARG, "%s: t_skip must be finite", fn);
+    if (dtype != RF_BF16)
+        return fail(RF_ERR_UNSUPPORTED, "%s: the projected keys and values are formed in bf16 attention only", fn);
+    if (cache->T != T || H <= 0 || W <= 0 || cache->rows_per_frame != static_cast<int64_t>(H) * W ||
+        heads <= 0 || head_dim <= 0 || cache->hidden != static_cast<int64_t>(heads) * head_dim ||
+        cache->dtype != dtype)
+        return fail(RF_ERR_INVALID_ARG,
+                    "%s: the cache (T=%d, %lld rows of %d, dtype %d) does not match the attention "
+                    "(T=%d, %d x %d rows of %d x %d, dtype %d)", fn, cache->T,
+                    static_cast<long long>(cache->rows_per_frame), cache->hidden, cache->dtype, T, H, W, heads,
+                    head_dim, dtype);
+    if (!workspace) return fail(RF_ERR_INVALID_ARG, "%s: NULL workspace", fn);
+    const CacheForm cf{cache, store, t_skip};
+    return attention_call(q, k, v, out, keyframe_ids, M, nullptr, 0, T, H, W, heads, head_dim, dtype, workspace,
+                          workspace_bytes, stream, fn, false, &cf);
 }
 
 // ---------------------------------------------------------------------------

@@ -43,9 +43,16 @@
 //    are then split along the keys into parts that run as extra workgroups;
 //    each part writes its unnormalised (O, m, l) in fp32, and a small kernel
 //    combines the parts of a tile (max of the references, rescaled sums).
-//  * Frame-level key/value mask (the kKvList form): the key loop walks a list
+//  * Frame-level key/value mask (the frame-list form): the key loop walks a list
 //    of frames in key tiles that never cross a frame; masked frames are
 //    never read.
+//  * Projected keys and values at a skipped step (the cache form; App. B.2):
+//    the key loop walks all frames in frame-aligned tiles; a tile of a cached
+//    frame loads that frame's two cached hidden states h_before and h_after
+//    instead of K and V, and the workgroup forms
+//    h = fmaf(alpha, h_after, (1 - alpha) h_before), rounded once to bf16, in
+//    LDS as both the key tile and the value tile, so the projected keys and
+//    values are never written to HBM.
 // The fp32 kernel at the end is a plain correctness path (fp32 throughout).
 #include <atomic>
 
@@ -130,8 +137,21 @@ struct AttnKArgs {
     // a frame (tiles_per_frame = ceil(N / key tile); a frame's last tile is partial)
     int32_t n_kv;
     int32_t tiles_per_frame;
+    // frame-list form: the listed frames; cache form (all T frames walked): per
+    // frame the two cache slots (h_before | h_after << 16), or -1 when the frame
+    // takes its keys and values from k and v
     int32_t kvf[kMaxFrames];
+    const uint16_t *store;           // cache form: [slot][N][heads][head_dim] cached hidden states
+    float calpha[kMaxFrames];        // cache form: each cached frame's weight alpha
 };
+
+// Kernel arguments travel in the kernarg segment: keep them within 4 KB.
+static_assert(sizeof(AttnKArgs) <= 4096, "attention kernel arguments exceed 4 KB");
+
+// Forms of the bf16 kernel's key loop.
+constexpr int kFormDense = 0;    // all S tokens in order
+constexpr int kFormFrames = 1;   // the tokens of the listed frames a.kvf
+constexpr int kFormCache = 2;    // all frames; cached frames give projected keys = values
 
 // Word 3 of a raw (untyped, stride 0) buffer resource on gfx9-class GPUs.
 constexpr int kBufferWord3 = 0x00020000;
@@ -296,11 +316,12 @@ __device__ __forceinline__ void pv_tile(const uint8_t *vb, const int (&vofs)[D /
 // range check zero-fills the keys past it (keys >= S, or past the end of a
 // frame in the frame-masked form) and their scores are masked. The loop is
 // unrolled by two so every LDS access names its buffer statically.
-// kKvList: the keys are the tokens of the frames a.kvf (a frame-level mask);
-// otherwise all S tokens in order.
-template <int D, bool kKvList>
+// kForm: kFormDense, kFormFrames (the keys are the tokens of the frames a.kvf,
+// a frame-level mask) or kFormCache (every frame, cached frames projected).
+template <int D, int kForm>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const AttnKArgs a) {
+    constexpr bool kKvList = kForm != kFormDense;   // frame-aligned tiles
     using L = TileLayout<D>;
     constexpr int kBc = L::kBc;
     constexpr int kNB = kBc / 32;                       // 32-key score blocks per tile
@@ -384,16 +405,31 @@ void attn_bf16_kernel(const AttnKArgs a) {
 
     // Tile t: its first key's token, the bytes from there to the end of its last
     // valid key, and the number of valid keys (at most kBc).
+    // Cache form: slots >= 0 for a tile of a cached frame (before | after << 16),
+    // its rows' offset inside the frame and the frame's weight.
     struct Geom {
         int64_t tok0, left;
         int32_t valid;
+        int32_t slots;
+        int64_t frame_off;
+        float alpha;
     };
     auto geom = [&](int64_t t) {
         Geom g;
+        g.slots = -1;
+        g.frame_off = 0;
+        g.alpha = 0.0f;
         if constexpr (kKvList) {
             const int32_t m = static_cast<int32_t>(t) / a.tiles_per_frame;
             const int64_t o = (t - static_cast<int64_t>(m) * a.tiles_per_frame) * kBc;
-            g.tok0 = static_cast<int64_t>(a.kvf[m]) * a.N + o;
+            if constexpr (kForm == kFormCache) {
+                g.tok0 = static_cast<int64_t>(m) * a.N + o;
+                g.slots = a.kvf[m];
+                g.frame_off = o;
+                g.alpha = a.calpha[m];
+            } else {
+                g.tok0 = static_cast<int64_t>(a.kvf[m]) * a.N + o;
+            }
             g.valid = static_cast<int32_t>(a.N - o < kBc ? a.N - o : kBc);
             g.left = ((g.valid - 1) * rs + D) * 2;
         } else {
@@ -409,6 +445,25 @@ void attn_bf16_kernel(const AttnKArgs a) {
         // key (clamped to 2^31 - 1: a tile never reaches that far past its first key).
         const int32_t rec = __builtin_amdgcn_readfirstlane(
             static_cast<int32_t>(g.left < 0x7fffffffLL ? g.left : 0x7fffffffLL));
+        if constexpr (kForm == kFormCache) {
+            if (g.slots >= 0) {
+                // a cached frame: h_before into the key buffer, h_after into the value
+                // buffer, both in the key layout (project_tile then writes both tiles)
+                const uint16_t *hb = a.store + ((g.slots & 0xffff) * a.N + g.frame_off) * rs + head * D;
+                const uint16_t *ha = a.store + ((g.slots >> 16) * a.N + g.frame_off) * rs + head * D;
+                const __amdgpu_buffer_rsrc_t br =
+                    __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(hb), 0, rec, kBufferWord3);
+                const __amdgpu_buffer_rsrc_t ar =
+                    __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(ha), 0, rec, kBufferWord3);
+#pragma unroll
+                for (int i = 0; i < kLoadsPerWave; ++i) {
+                    const int chunk = (wave * kLoadsPerWave + i) * 1024;
+                    load_lds16(br, (lds_void_t *)(kdst + chunk), kgo[i]);
+                    load_lds16(ar, (lds_void_t *)(vdst + chunk), kgo[i]);
+                }
+                return;
+            }
+        }
         const __amdgpu_buffer_rsrc_t kr =
             __builtin_amdgcn_make_buffer_rsrc(uniform_ptr(kbase + g.tok0 * rs), 0, rec, kBufferWord3);
         const __amdgpu_buffer_rsrc_t vr =
@@ -418,6 +473,57 @@ void attn_bf16_kernel(const AttnKArgs a) {
             const int chunk = (wave * kLoadsPerWave + i) * 1024;
             load_lds16(kr, (lds_void_t *)(kdst + chunk), kgo[i]);
             load_lds16(vr, (lds_void_t *)(vdst + chunk), vgo[i]);
+        }
+    };
+
+    // Cache form: the projected state of a cached frame's tile, formed in LDS.
+    // The key buffer holds h_before and the value buffer h_after, both in the key
+    // layout; each wave owns whole key rows (kBc / 8 of them), reads its rows' 16-byte
+    // slots of both, and writes h = fmaf(alpha, h_after, (1 - alpha) h_before),
+    // rounded once to bf16, back into the key buffer at the same slot and into the
+    // value buffer at the slot the value layout puts it. A wave's LDS instructions
+    // run in order and no other wave touches its rows, so its reads see the loaded
+    // states before its writes replace them. The caller's barrier then publishes
+    // both tiles.
+    auto project_tile = [&](uint8_t *kb, uint8_t *vb, float alpha) {
+        constexpr int kRowsPerWave = kBc / kWaves;
+        constexpr int kPerLane = kRowsPerWave * L::kSlots / 64;
+        static_assert(kRowsPerWave * L::kSlots % 64 == 0, "a wave's rows must split evenly over its lanes");
+        const float oma = 1.0f - alpha;
+        u32x4_t hv[kPerLane];
+        int pk[kPerLane], pv[kPerLane];
+#pragma unroll
+        for (int i = 0; i < kPerLane; ++i) {
+            const int sidx = lane * kPerLane + i;
+            const int key = wave * kRowsPerWave + sidx / L::kSlots;
+            const int slot = sidx % L::kSlots;
+            pk[i] = key * L::kRow + (slot ^ L::kswz(key)) * 16;
+            pv[i] = key * L::kRow + (slot ^ L::vswz(key)) * 16;
+            const u32x4_t b = *reinterpret_cast<const u32x4_t *>(kb + pk[i]);
+            const u32x4_t af = *reinterpret_cast<const u32x4_t *>(vb + pk[i]);
+            u32x4_t h;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float lo = fmaf(alpha, __uint_as_float(af[e] << 16), oma * __uint_as_float(b[e] << 16));
+                const float hi = fmaf(alpha, __uint_as_float(af[e] & 0xffff0000u),
+                                      oma * __uint_as_float(b[e] & 0xffff0000u));
+                h[e] = pack_bf16x2(lo, hi);
+            }
+            hv[i] = h;
+        }
+#pragma unroll
+        for (int i = 0; i < kPerLane; ++i) {
+            *reinterpret_cast<u32x4_t *>(kb + pk[i]) = hv[i];
+            *reinterpret_cast<u32x4_t *>(vb + pv[i]) = hv[i];
+        }
+    };
+    // after a tile's loads are visible: form the projected tile if the frame is cached
+    auto settle_tile = [&](const Geom &g, uint8_t *kb, uint8_t *vb) {
+        if constexpr (kForm == kFormCache) {
+            if (g.slots >= 0) {
+                project_tile(kb, vb, g.alpha);
+                __syncthreads();
+            }
         }
     };
 
@@ -504,6 +610,7 @@ void attn_bf16_kernel(const AttnKArgs a) {
     Geom cur = geom(t_begin);
     issue(cur, k0, v0);
     tile_done();
+    settle_tile(cur, k0, v0);
     for (int64_t t = t_begin; t < t_end; t += 2) {
         Geom nxt = cur;
         if (t + 1 < t_end) {
@@ -513,12 +620,16 @@ void attn_bf16_kernel(const AttnKArgs a) {
         compute(cur.valid, k0, v0);
         tile_done();
         if (t + 1 >= t_end) break;
+        // (a projected tile is formed while no load is in flight, so its barrier
+        // waits for nothing but the projection itself)
+        settle_tile(nxt, k1, v1);
         if (t + 2 < t_end) {
             cur = geom(t + 2);
             issue(cur, k0, v0);
         }
         compute(nxt.valid, k1, v1);
         tile_done();
+        if (t + 2 < t_end) settle_tile(cur, k0, v0);
     }
 
     l_run = halves_sum(l_run);
@@ -742,7 +853,7 @@ hipError_t device_geometry(DeviceGeometry *out) {
 }
 
 AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv,
-                          int32_t cus) {
+                          int32_t cus, int32_t walk_frames) {
     AttnSplit sp{};
     const int64_t total = (Mq + kBr - 1) / kBr * heads;
     const int64_t kBc = key_tile(head_dim);
@@ -765,7 +876,9 @@ AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N
     sp.n_direct = total - tail;
     sp.n_tail = tail;
     sp.split = best_s;
-    sp.kv_per_split = (kv_tiles + best_s - 1) / best_s;
+    // a frame-aligned walk has at least as many key tiles, so its parts keep >= kMinKvPerSplit
+    const int64_t walk = walk_frames > 0 ? static_cast<int64_t>(walk_frames) * ((N + kBc - 1) / kBc) : kv_tiles;
+    sp.kv_per_split = (walk + best_s - 1) / best_s;
     sp.ws_bytes = tail * best_s * kBr * (static_cast<int64_t>(head_dim) * 4 + 8);
     return sp;
 }
@@ -787,8 +900,9 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         if (p.geo.cus < 1 || xcds < 1 || xcds > 64) return hipErrorInvalidValue;
         AttnSplit sp{};
         sp.n_direct = nq * p.heads;
+        const int32_t walk = p.cache_form ? static_cast<int32_t>(p.S / p.N) : 0;
         if (p.ws) {
-            sp = attention_split(Mq, p.heads, p.head_dim, p.N, p.S, p.n_kv, p.geo.cus);
+            sp = attention_split(Mq, p.heads, p.head_dim, p.N, p.S, p.n_kv, p.geo.cus, walk);
             if (sp.split > 0 && p.ws_bytes < sp.ws_bytes) return hipErrorInvalidValue;
         }
         const int64_t total = sp.n_direct;
@@ -814,15 +928,26 @@ hipError_t launch_attention(const AttnParams &p, hipStream_t stream) {
         a.n_kv = p.n_kv;
         a.tiles_per_frame = static_cast<int32_t>((p.N + kBc - 1) / kBc);
         for (int i = 0; i < p.n_kv; ++i) a.kvf[i] = p.kvf[i];
-        if (p.n_kv > 0 && static_cast<int64_t>(p.n_kv) * a.tiles_per_frame > 0x7fffffffLL)
+        if (p.cache_form) {
+            a.n_kv = walk;
+            for (int i = 0; i < walk; ++i) {
+                a.kvf[i] = p.cslot[i];
+                a.calpha[i] = p.calpha[i];
+            }
+            a.store = static_cast<const uint16_t *>(p.store);
+        }
+        if (a.n_kv > 0 && static_cast<int64_t>(a.n_kv) * a.tiles_per_frame > 0x7fffffffLL)
             return hipErrorInvalidConfiguration;
         const dim3 grid(static_cast<uint32_t>(per_xcd * xcds + n_parts)), block(kThreads);
-        if (p.n_kv > 0) {
-            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, stream, a);
+        if (p.cache_form) {
+            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, kFormCache>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, kFormCache>), grid, block, 0, stream, a);
+        } else if (p.n_kv > 0) {
+            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, kFormFrames>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, kFormFrames>), grid, block, 0, stream, a);
         } else {
-            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, stream, a);
-            else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, stream, a);
+            if (p.head_dim == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, kFormDense>), grid, block, 0, stream, a);
+            else hipLaunchKernelGGL((attn_bf16_kernel<64, kFormDense>), grid, block, 0, stream, a);
         }
         if (sp.split == 0) return hipGetLastError();
         const hipError_t e = hipGetLastError();

@@ -37,6 +37,13 @@ struct AttnParams {
     // 0: keys are all S tokens; > 0: only the tokens of frames kvf[0..n_kv)
     int32_t n_kv;
     int32_t kvf[kMaxFrames];
+    // cache form (bf16): every frame walked; frame f with cslot[f] >= 0 takes
+    // the projection of store slots (cslot & 0xffff, cslot >> 16) with weight
+    // calpha[f] as its keys and values
+    int32_t cache_form;
+    const void *store;
+    int32_t cslot[kMaxFrames];
+    float calpha[kMaxFrames];
     // optional workspace for the split-key tail (NULL: no split)
     void *ws;
     int64_t ws_bytes;
@@ -56,8 +63,10 @@ struct AttnSplit {
     int64_t ws_bytes;
 };
 
+// walk_frames > 0: the key loop walks that many whole frames in frame-aligned
+// tiles (the cache form) while the number of parts is chosen as for n_kv.
 AttnSplit attention_split(int64_t Mq, int32_t heads, int32_t head_dim, int64_t N, int64_t S, int32_t n_kv,
-                          int32_t cus);
+                          int32_t cus, int32_t walk_frames = 0);
 
 
 hipError_t launch_attention(const AttnParams &p, hipStream_t stream);
