@@ -572,8 +572,9 @@ def measured_peaks(attn_tflops):
     instruction to the next, 4 workgroups of 4 waves per compute unit, launches
     back to back, the second half averaged; the clock it implies at 4096 FLOP
     per CU and cycle; the same on zero operands, which do not toggle), the
-    vendor library's 8192^3 bf16 product as a reference point, and HBM reads
-    (2 GiB, far beyond the 256 MB Infinity Cache, best of three grid sizes)."""
+    vendor library's 8192^3 bf16 product as a reference point, HBM reads
+    (2 GiB, far beyond the 256 MB Infinity Cache, best of three grid sizes),
+    and LDS reads (16-byte and transposing 8-byte, at 8 waves per CU)."""
     import torch
     from paper_2606_06309_amd import binding as rf
 
@@ -625,9 +626,38 @@ def measured_peaks(attn_tflops):
         best = max(best, (gbs, wgr))
         del sink
     del src
+
+    # LDS reads: two workgroups of 4 waves per CU (the attention kernel's 8 waves), each
+    # wave reading its workgroup's 64 KB per round. The longest workgroup's shader-clock
+    # ticks span (nearly) the whole launch: the clock is those ticks over the event time,
+    # and bytes per clock per CU the launch's bytes over CUs x those ticks.
+    lds = {}
+    lwg, lrounds = 512, 4000
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for width in (16, 8):
+        sink, ticks = rf.rf_probe_lds_read(lwg, 2, width)
+        torch.cuda.synchronize()
+        ev = _events(6)
+        for a, b in ev:
+            a.record()
+            rf.rf_probe_lds_read(lwg, lrounds, width, sink=sink, ticks=ticks)
+            b.record()
+        torch.cuda.synchronize()
+        ms = _avg_ms(ev[3:])
+        tk = ticks.double()
+        tmax, tmin = float(tk.max().item()), float(tk.min().item())
+        nbytes_l = lwg * 4 * lrounds * 65536
+        lds[f"width_{width}"] = {
+            "tbs": round(nbytes_l / (ms * 1e-3) / 1e12, 2),
+            "bytes_per_clk_per_cu": round(nbytes_l / (cus * tmax), 1),
+            "clock_ghz_from_ticks": round(tmax / (ms * 1e-3) / 1e9, 3),
+            "workgroup_ticks_min_over_max": round(tmin / tmax, 3),
+            "read": "16-byte" if width == 16 else "transposing 8-byte"}
+        del sink, ticks
     print(f"[bench] measured peaks: bf16 MFMA {mfma_tf:.0f} TFLOP/s on random operands (clock {clock:.2f} GHz), "
-          f"{mfma_zero_tf:.0f} on zero operands; library GEMM {gemm_tf:.0f}; HBM read {best[0]:.0f} GB/s",
-          file=sys.stderr, flush=True)
+          f"{mfma_zero_tf:.0f} on zero operands; library GEMM {gemm_tf:.0f}; HBM read {best[0]:.0f} GB/s; "
+          f"LDS {lds['width_16']['bytes_per_clk_per_cu']} B/clk/CU (16-byte), "
+          f"{lds['width_8']['bytes_per_clk_per_cu']} (transposing 8-byte)", file=sys.stderr, flush=True)
     return {"mfma_bf16": {"tflops": round(mfma_tf, 1), "spec_tflops": PEAK_BF16_TFLOPS,
                           "frac_spec": round(mfma_tf / PEAK_BF16_TFLOPS, 4), "clock_ghz": round(clock, 3),
                           "workgroups": wg, "rounds": rounds, "operands": "random normal bf16",
@@ -636,6 +666,7 @@ def measured_peaks(attn_tflops):
                                   "call": "torch.matmul, random normal bf16"},
             "hbm_read": {"gbs": round(best[0], 1), "spec_gbs": PEAK_HBM_GBS,
                          "frac_spec": round(best[0] / PEAK_HBM_GBS, 4), "bytes": nbytes, "workgroups": best[1]},
+            "lds_read": dict(lds, workgroups=lwg, rounds=lrounds, compute_units=cus),
             "attention_frac_of_measured_mfma": round(attn_tflops / mfma_tf, 4)}
 
 

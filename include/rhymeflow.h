@@ -12,9 +12,9 @@
  * them, the content-aware keyframe selection of Sec. 3.1 (frame similarity and
  * Alg. 1's scan), the per-layer rolling cache of App. B.2, whose projected
  * hidden states are the skipped frames' keys and values, and the progressive
- * asynchronous schedule (Eq. 2, Alg. 2) that says which step is which. Two
+ * asynchronous schedule (Eq. 2, Alg. 2) that says which step is which. Three
  * device probes, measurement support outside the method, report the rates the
- * matrix cores and HBM sustain on this device.
+ * matrix cores, LDS and HBM sustain on this device.
  *
  * Conventions shared by every call:
  *  - Return value: RF_OK (0) or a negative rf_status. No C++ exception crosses
@@ -559,7 +559,7 @@ int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, in
  * set a kernel's achieved rate against what the device delivers besides the
  * published peaks (MI355X: dense bf16 matrix 2.5 PFLOP/s at 2.4 GHz, HBM3E
  * 8 TB/s); the chip runs below that clock when all matrix cores are busy.
- * Both enqueue one kernel on `stream` and return at once; time them with
+ * Each enqueues one kernel on `stream` and returns at once; time them with
  * events on that stream. Workgroups have 256 threads.
  */
 
@@ -584,6 +584,32 @@ int rf_async_schedule(int32_t T, int32_t T_w, int32_t T_mid, int32_t n_small, in
  * (workgroups, rounds), RF_ERR_UNSUPPORTED (alignment).
  */
 int rf_probe_mfma_bf16(const void *operands, int32_t workgroups, int32_t rounds, float *sink, void *stream);
+
+/*
+ * LDS reads: each of a workgroup's 4 waves reads the workgroup's 64 KB LDS
+ * array (32-bit word i holds i * 2654435761 mod 2^32) in full `rounds` times,
+ * with 16-byte reads (width 16) or with the transposing 8-byte reads of 16-bit
+ * elements (width 8, the form that reads V^T operands for the matrix cores).
+ * Width 16: round r reads the 64 rows of 1 KB in order, lane l at bytes
+ * 16 ((l + r) % 64) .. +16 of each. Width 8: the array is 256 rows of 256
+ * bytes; read t (0..127) of round r gives lane 16h + 4q + e (h, q, e = 0..3)
+ * the 8 bytes at row 8 (t / 4) + 4 (h / 2) + q, byte
+ * 32 ((2 ((t + r) % 4) + h % 2) XOR 2q) + 8e, which the hardware redistributes
+ * within each group of 16 lanes (the layout the attention kernel reads V tiles
+ * in). 64 KB of LDS per workgroup puts two workgroups on a compute unit.
+ * Bytes per launch: workgroups * 4 * rounds * 65536.
+ * sink: device uint32 [workgroups * 256], 4-byte aligned. Width 16: thread i
+ * (lane l) writes the sum mod 2^32 of the 32-bit words it read. Width 8: a
+ * thread writes the XOR of the 32-bit words it received; over a group of 16
+ * lanes, that XOR folded to 16 bits (low half XOR high half) is the XOR of the
+ * 16-bit elements the group addressed.
+ * ticks: NULL, or device uint64 [workgroups], 8-byte aligned: the shader-clock
+ * ticks (s_memtime) each workgroup spent between the barriers around its reads.
+ * workgroups 1..2^20, rounds 1..2^22. Errors: RF_ERR_INVALID_ARG (NULL sink,
+ * width), RF_ERR_RANGE (workgroups, rounds), RF_ERR_UNSUPPORTED (alignment).
+ */
+int rf_probe_lds_read(int32_t workgroups, int32_t rounds, int32_t width, uint32_t *sink, uint64_t *ticks,
+                      void *stream);
 
 /*
  * HBM reads: the workgroups read the device buffer src of `bytes` bytes once

@@ -37,7 +37,7 @@ EXPORTED = [
     "rf_frame_similarity", "rf_frame_similarity_workspace", "rf_select_keyframes_adaptive",
     "rf_cache_store_bytes", "rf_cache_init", "rf_cache_shift_store", "rf_cache_alpha",
     "rf_cache_project_kv", "rf_keyframe_attention_cached", "rf_async_schedule",
-    "rf_probe_mfma_bf16", "rf_probe_hbm_read",
+    "rf_probe_mfma_bf16", "rf_probe_hbm_read", "rf_probe_lds_read",
 ]
 
 RF_STEP_WARMUP = 0
@@ -176,6 +176,8 @@ lib.rf_probe_mfma_bf16.argtypes = [_vp, _i32, _i32, _vp, _vp]
 lib.rf_probe_mfma_bf16.restype = ctypes.c_int
 lib.rf_probe_hbm_read.argtypes = [_vp, _i64, _i32, _vp, _vp]
 lib.rf_probe_hbm_read.restype = ctypes.c_int
+lib.rf_probe_lds_read.argtypes = [_i32, _i32, _i32, _vp, _vp, _vp]
+lib.rf_probe_lds_read.restype = ctypes.c_int
 
 
 def _check(status: int):
@@ -674,3 +676,23 @@ def rf_probe_hbm_read(src: torch.Tensor, workgroups: int, sink=None, stream=None
     _check(lib.rf_probe_hbm_read(_dev(src, "src"), src.numel() * src.element_size(), workgroups,
                                  _dev(sink, "sink"), _stream(stream)))
     return sink
+
+
+def rf_probe_lds_read(workgroups: int, rounds: int, width: int = 16, sink=None, ticks=None, device="cuda",
+                      stream=None):
+    """Enqueues the LDS read probe (workgroups * 4 * rounds * 64 KB read from
+    LDS, 16-byte reads for width 16, transposing 8-byte reads for width 8);
+    returns (sink, ticks): int32 [workgroups * 256] sums and int64
+    [workgroups] shader-clock ticks of each workgroup's reads."""
+    dev = torch.device(device)
+    if sink is None:
+        sink = _empty(workgroups * PROBE_THREADS, torch.int32, dev, stream)
+    if ticks is None:
+        ticks = _empty(workgroups, torch.int64, dev, stream)
+    if sink.element_size() != 4 or sink.numel() < workgroups * PROBE_THREADS:
+        raise ValueError("sink must have 4-byte elements, workgroups * 256 of them")
+    if ticks.element_size() != 8 or ticks.numel() < workgroups:
+        raise ValueError("ticks must have 8-byte elements, workgroups of them")
+    _check(lib.rf_probe_lds_read(workgroups, rounds, width, _dev(sink, "sink"), _dev(ticks, "ticks"),
+                                 _stream(stream)))
+    return sink, ticks

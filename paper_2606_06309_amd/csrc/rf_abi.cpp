@@ -863,6 +863,20 @@ int rf_probe_mfma_bf16(const void *operands, int32_t workgroups, int32_t rounds,
                     fn);
 }
 
+int rf_probe_lds_read(int32_t workgroups, int32_t rounds, int32_t width, uint32_t *sink, uint64_t *ticks,
+                      void *stream) {
+    const char *fn = "rf_probe_lds_read";
+    if (!sink) return fail(RF_ERR_INVALID_ARG, "%s: NULL sink", fn);
+    if (width != 16 && width != 8) return fail(RF_ERR_INVALID_ARG, "%s: width %d is not 16 or 8", fn, width);
+    if (workgroups < 1 || workgroups > (1 << 20) || rounds < 1 || rounds > (1 << 22))
+        return fail(RF_ERR_RANGE, "%s: workgroups %d (1..2^20) or rounds %d (1..2^22) out of range", fn,
+                    workgroups, rounds);
+    if ((reinterpret_cast<uintptr_t>(sink) & 3u) || (reinterpret_cast<uintptr_t>(ticks) & 7u))
+        return fail(RF_ERR_UNSUPPORTED, "%s: sink must be 4-byte and ticks 8-byte aligned", fn);
+    return launched(
+        rf::launch_lds_read_probe(workgroups, rounds, width, sink, ticks, static_cast<hipStream_t>(stream)), fn);
+}
+
 int rf_probe_hbm_read(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink, void *stream) {
     const char *fn = "rf_probe_hbm_read";
     if (!src || !sink) return fail(RF_ERR_INVALID_ARG, "%s: NULL argument", fn);

@@ -153,6 +153,8 @@ hipError_t launch_similarity(const SimParams &p, hipStream_t stream);
 constexpr int kProbeThreads = 256;
 hipError_t launch_mfma_probe(const void *ops, int32_t workgroups, int32_t rounds, float *sink,
                              hipStream_t stream);
+hipError_t launch_lds_read_probe(int32_t workgroups, int32_t rounds, int32_t width, uint32_t *sink,
+                                 uint64_t *ticks, hipStream_t stream);
 hipError_t launch_hbm_read_probe(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink,
                                  hipStream_t stream);
 

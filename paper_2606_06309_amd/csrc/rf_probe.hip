@@ -21,6 +21,13 @@
 //  * hbm_read_kernel: a grid-stride read of 16-byte words (four loads in
 //    flight per thread), folded with XOR into one 32-bit word per thread, so
 //    the XOR of all sink words equals the XOR of all words of the buffer.
+//  * lds_read_kernel: every wave of a workgroup reads a 64 KB LDS array in
+//    full per round, with 16-byte reads or with the transposing 8-byte reads
+//    the attention kernel takes its V^T operands with, as many in flight as
+//    the compiler keeps, and adds what it reads into two 32-bit sums. The workgroup's elapsed
+//    shader-clock ticks over its read loop give the bytes per clock; 64 KB of
+//    LDS per workgroup puts two workgroups (8 waves) on a compute unit, the
+//    attention kernel's occupancy.
 #include "rf_internal.h"
 
 namespace rf {
@@ -83,7 +90,78 @@ __global__ __launch_bounds__(kProbeThreads) void hbm_read_kernel(const u32x4_t *
     sink[static_cast<int64_t>(blockIdx.x) * kProbeThreads + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
 }
 
+constexpr int kLdsWords = 16384;   // 64 KB of LDS per workgroup
+
+// The 16-byte form reads the array row by row (64 rows of 64 lanes x 16
+// bytes), lane l in round r at column (l + r) % 64, and sums 32-bit words.
+// The transposing form addresses LDS as the attention kernel addresses a V
+// tile of 256-byte key rows: in read t of round r, lanes 16h + 4q + e (h = 0..3,
+// q, e = 0..3) take the 8 bytes at row 8 (t / 4) + 4 (h / 2) + q, 32-byte chunk
+// (2 ((t + r) % 4) + h % 2) ^ 2q, byte 8e, so the 16 lanes of a group cover
+// 4 rows x 32 bytes and a wave 8 rows x 64 bytes; the hardware hands lane
+// 16h + i the i-th 16-bit element of each of the group's 4 rows. That form
+// XORs the 32-bit words it receives: a group's XOR, folded to 16 bits (low half
+// XOR high half), is the XOR of the 16-bit elements the group addressed however
+// they are distributed. Either way each round of each wave reads every byte once
+// and a lane's bytes change from round to round.
+template <int kWidth>
+__global__ __launch_bounds__(kProbeThreads) void lds_read_kernel(int32_t rounds, uint32_t *sink,
+                                                                 uint64_t *ticks) {
+    __shared__ __attribute__((aligned(16))) uint32_t buf[kLdsWords];
+    for (int i = threadIdx.x; i < kLdsWords; i += kProbeThreads) buf[i] = static_cast<uint32_t>(i) * 2654435761u;
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const uint8_t *base = reinterpret_cast<const uint8_t *>(buf);
+    uint32_t s0 = 0u, s1 = 0u;
+    const uint64_t t0 = __builtin_amdgcn_s_memtime();
+    if constexpr (kWidth == 16) {
+        for (int32_t r = 0; r < rounds; ++r) {
+            const uint8_t *col = base + ((lane + r) & 63) * 16;
+#pragma unroll
+            for (int j = 0; j < 64; ++j) {
+                const u32x4_t w = *reinterpret_cast<const u32x4_t *>(col + j * 1024);
+                s0 += w[0] + w[1];
+                s1 += w[2] + w[3];
+            }
+        }
+    } else {
+        typedef short i16x4_t __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+        typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+        const int h = lane >> 4, q = (lane >> 2) & 3, e = lane & 3;
+        const int row_ofs = (4 * (h >> 1) + q) * 256 + 8 * e;
+        for (int32_t r = 0; r < rounds; ++r) {
+            int po[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) po[p] = row_ofs + (((2 * ((p + r) & 3) + (h & 1)) ^ (2 * q)) * 32);
+#pragma unroll
+            for (int t = 0; t < 128; ++t) {
+                const i16x4_t v =
+                    __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(base + (t / 4) * 2048 + po[t % 4]));
+                const u32x2_t w = __builtin_bit_cast(u32x2_t, v);
+                s0 ^= w[0];
+                s1 ^= w[1];
+            }
+        }
+    }
+    __syncthreads();
+    const uint64_t t1 = __builtin_amdgcn_s_memtime();
+    sink[static_cast<int64_t>(blockIdx.x) * kProbeThreads + threadIdx.x] = kWidth == 16 ? s0 + s1 : s0 ^ s1;
+    if (ticks && threadIdx.x == 0) ticks[blockIdx.x] = t1 - t0;
+}
+
 }  // namespace
+
+hipError_t launch_lds_read_probe(int32_t workgroups, int32_t rounds, int32_t width, uint32_t *sink,
+                                 uint64_t *ticks, hipStream_t stream) {
+    if (width == 16)
+        hipLaunchKernelGGL(lds_read_kernel<16>, dim3(static_cast<uint32_t>(workgroups)), dim3(kProbeThreads), 0,
+                           stream, rounds, sink, ticks);
+    else
+        hipLaunchKernelGGL(lds_read_kernel<8>, dim3(static_cast<uint32_t>(workgroups)), dim3(kProbeThreads), 0,
+                           stream, rounds, sink, ticks);
+    return hipGetLastError();
+}
 
 hipError_t launch_mfma_probe(const void *ops, int32_t workgroups, int32_t rounds, float *sink,
                              hipStream_t stream) {

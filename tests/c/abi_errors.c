@@ -253,6 +253,11 @@ int main(void) {
     EXPECT(rf_probe_mfma_bf16(DEV(0), 0, 1, (float *)DEV(1), NULL), RF_ERR_RANGE);
     EXPECT(rf_probe_hbm_read(DEV(0), 17, 1, (uint32_t *)DEV(1), NULL), RF_ERR_INVALID_ARG);
     EXPECT(rf_probe_hbm_read(DEV(0), 4096, 0, (uint32_t *)DEV(1), NULL), RF_ERR_RANGE);
+    EXPECT(rf_probe_lds_read(1, 1, 16, NULL, NULL, NULL), RF_ERR_INVALID_ARG);
+    EXPECT(rf_probe_lds_read(1, 1, 12, (uint32_t *)DEV(1), NULL, NULL), RF_ERR_INVALID_ARG);
+    EXPECT(rf_probe_lds_read(1, 0, 8, (uint32_t *)DEV(1), NULL, NULL), RF_ERR_RANGE);
+    EXPECT(rf_probe_lds_read(1, 1, 8, (uint32_t *)DEV(1), (uint64_t *)((char *)DEV(0) + 4), NULL),
+           RF_ERR_UNSUPPORTED);
 
     /* every status has a name; an unknown one too */
     for (int s = -6; s <= 1; ++s)

@@ -341,6 +341,23 @@ def test_hbm_probe_validation(args, status):
     assert lib.rf_probe_hbm_read(a["src"], a["nbytes"], a["wg"], a["sink"], None) == status
 
 
+@pytest.mark.parametrize("args,status", [
+    (dict(sink=None), rf.RF_ERR_INVALID_ARG),
+    (dict(width=4), rf.RF_ERR_INVALID_ARG),
+    (dict(width=32), rf.RF_ERR_INVALID_ARG),
+    (dict(wg=0), rf.RF_ERR_RANGE),
+    (dict(wg=(1 << 20) + 1), rf.RF_ERR_RANGE),
+    (dict(rounds=0), rf.RF_ERR_RANGE),
+    (dict(rounds=(1 << 22) + 1), rf.RF_ERR_RANGE),
+    (dict(sink=B_ + 2), rf.RF_ERR_UNSUPPORTED),
+    (dict(ticks=A + 4), rf.RF_ERR_UNSUPPORTED),
+])
+def test_lds_probe_validation(args, status):
+    a = dict(wg=4, rounds=8, width=16, sink=B_, ticks=A)
+    a.update(args)
+    assert lib.rf_probe_lds_read(a["wg"], a["rounds"], a["width"], a["sink"], a["ticks"], None) == status
+
+
 def test_sizes_overflowing_byte_counts_are_range_errors():
     """Sizes whose byte counts would pass 64 bits are rejected before any is
     formed in integers (and before any HIP call)."""

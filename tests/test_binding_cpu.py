@@ -29,6 +29,7 @@ CALLS = {
                                                 sink=torch.zeros(256)),
     "probe_hbm": lambda: rf.rf_probe_hbm_read(torch.zeros(4096, dtype=torch.uint8), 1,
                                               sink=torch.zeros(256, dtype=torch.int32)),
+    "probe_lds": lambda: rf.rf_probe_lds_read(1, 1, 16, device="cpu"),
 }
 
 

@@ -6,7 +6,13 @@ B element (k, n) in lane n + 32 (k/8), accumulator r of lane l = element
 (8 (r/4) + 4 (l/32) + r%4, l%32)); all-ones operands give the closed form
 8192 per round. HBM read probe: the XOR of its sink equals the XOR of every
 32-bit word of the buffer (numpy over the same bytes), on sizes with ragged
-tails."""
+tails. LDS read probe: with 16-byte reads each thread's sum equals the numpy
+sum of the words its lane's columns hold over the rounds; with transposing
+8-byte reads (which redistribute 16-bit elements within 16-lane groups) the
+XOR over each group of 16 lanes, folded to 16 bits, equals the numpy XOR of
+the 16-bit elements those lanes addressed, in the V-tile layout of the
+attention kernel (odd round counts: over an even count a group's XOR
+cancels)."""
 import numpy as np
 import pytest
 import torch
@@ -76,3 +82,52 @@ def test_hbm_read_probe_xor(nbytes, wg):
     got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     want = np.bitwise_xor.reduce(host.numpy().view(np.uint32))
     assert got == want
+
+
+LDS_WORDS = (np.arange(16384, dtype=np.uint64) * 2654435761) % (1 << 32)   # the probe's array
+
+
+def _lds_thread_sums_16(rounds):
+    """Per-lane sums of the 16-byte form: lane l reads, in round r, column
+    (l + r) % 64 (16 bytes = 4 words) of each of the 64 rows of 1 KB."""
+    col = LDS_WORDS.reshape(64, 64, 4).sum(axis=(0, 2))   # [column]
+    return np.array([sum(int(col[(l + r) % 64]) for r in range(rounds)) % (1 << 32) for l in range(64)],
+                    dtype=np.uint64)
+
+
+def _lds_group_xors_8(rounds):
+    """Per 16-lane group of the transposing 8-byte form: the XOR of the 16-bit
+    elements at the bytes the group's lanes address (the addressing the header
+    states), over all reads of all rounds."""
+    halves = LDS_WORDS.astype(np.uint32).view(np.uint16)   # 16-bit elements in address order
+    out = np.zeros(4, dtype=np.uint64)
+    for lane in range(64):
+        h, q, e = lane >> 4, (lane >> 2) & 3, lane & 3
+        for r in range(rounds):
+            for t in range(128):
+                byte = (8 * (t // 4) + 4 * (h // 2) + q) * 256 + ((2 * ((t + r) % 4) + h % 2) ^ (2 * q)) * 32 + 8 * e
+                out[h] ^= int(np.bitwise_xor.reduce(halves[byte // 2:byte // 2 + 4]))
+    return out
+
+
+@pytest.mark.parametrize("wg,rounds", [(1, 1), (3, 5), (512, 3)])
+def test_lds_read_probe_16_byte_sums(wg, rounds):
+    print(f"[case] lds read probe width 16 wg={wg} rounds={rounds}", flush=True)
+    sink, ticks = rf.rf_probe_lds_read(wg, rounds, 16)
+    torch.cuda.synchronize()
+    got = sink.cpu().numpy().view(np.uint32).astype(np.uint64).reshape(wg, 4, 64)
+    want = _lds_thread_sums_16(rounds)
+    assert (got == want[None, None, :]).all()
+    assert bool((ticks.cpu() > 0).all())
+
+
+@pytest.mark.parametrize("wg,rounds", [(1, 1), (2, 5), (512, 3)])
+def test_lds_read_probe_transposing_group_xors(wg, rounds):
+    print(f"[case] lds read probe width 8 wg={wg} rounds={rounds}", flush=True)
+    sink, ticks = rf.rf_probe_lds_read(wg, rounds, 8)
+    torch.cuda.synchronize()
+    words = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32).reshape(wg, 4, 4, 16), axis=3)
+    got = ((words & 0xffff) ^ (words >> 16)).astype(np.uint64)
+    want = _lds_group_xors_8(rounds)
+    assert (got == want[None, None, :]).all()
+    assert bool((ticks.cpu() > 0).all())
