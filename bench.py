@@ -411,13 +411,35 @@ def other_configs(headline, args):
     return res
 
 
+def _gpu_rows(w, q, k, v, pair_rows, pair_heads):
+    """The GPU's keyframe-query attention output (the timed call, split-key
+    tail included) on the oracle's own inputs q, k, v (host tensors, copied
+    to the device bit for bit) at the listed (compact row, head) pairs, as
+    exact float64."""
+    import numpy as np
+    import torch
+    from paper_2606_06309_amd import binding as rf
+
+    q, k, v = (x.cuda() for x in (q, k, v))
+    out = rf.rf_keyframe_attention_ws(q, k, v, list(w.keyframes), w.T, w.H, w.W)
+    torch.cuda.synchronize()
+    sel = out[torch.as_tensor(pair_rows, device="cuda"), torch.as_tensor(pair_heads, device="cuda")]
+    if sel.dtype == torch.bfloat16:
+        bits = sel.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+        return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return sel.cpu().double().numpy()
+
+
 def cpu_per_config(gpu_tflops):
     """The oracle per configuration, as the CPU baseline plan states it: the tiny
     workload in full; the small workload one head in full (all 7,800 rows over
     20,280 keys) extrapolated to its 12 heads; the larger ones on seeded row
     samples extrapolated to every (row, head) pair (each costs exactly 4*S*d
     FLOP); the projection oracle on the 480p latents and the selection oracle
-    (frame cosine on the long workload's latent grid plus Alg. 1's scan) in full."""
+    (frame cosine on the long workload's latent grid plus Alg. 1's scan) in full.
+    The oracle rows computed for the timing also give each configuration's
+    error statistics: the GPU's output at the same (row, head) pairs against
+    them (max and mean absolute error, relative Frobenius error)."""
     import numpy as np
     import oracle
     from paper_2606_06309_amd import accounting, workloads
@@ -430,17 +452,18 @@ def cpu_per_config(gpu_tflops):
         q, k, v = workloads.make_qkv(w)
         rowmap = oracle.rowmap(w.keyframes, w.N)
         if how is None:
-            toks, heads = np.repeat(rowmap, w.heads), np.tile(np.arange(w.heads), rowmap.size)
+            rows, heads = np.repeat(np.arange(rowmap.size), w.heads), np.tile(np.arange(w.heads), rowmap.size)
             label = "in full"
         elif how == "one head":
-            toks, heads = rowmap, np.zeros(rowmap.size, dtype=np.int64)
+            rows, heads = np.arange(rowmap.size), np.zeros(rowmap.size, dtype=np.int64)
             label = f"head 0 in full ({rowmap.size} rows), extrapolated to {w.heads} heads"
         else:
             rows = np.concatenate([rng.choice(rowmap.size, how, replace=False) for _ in range(w.heads)])
-            toks, heads = rowmap[rows], np.repeat(np.arange(w.heads), how)
-            label = f"{how} random rows per head ({toks.size} pairs), extrapolated to {rowmap.size * w.heads} pairs"
+            heads = np.repeat(np.arange(w.heads), how)
+            label = f"{how} random rows per head ({rows.size} pairs), extrapolated to {rowmap.size * w.heads} pairs"
+        toks = rowmap[rows]
         t0 = time.perf_counter()
-        oracle.attention_pairs(q, k, v, toks, heads)
+        ref = oracle.attention_pairs(q, k, v, toks, heads)
         dt = time.perf_counter() - t0
         pairs_total = rowmap.size * w.heads
         sec = dt * pairs_total / toks.size
@@ -451,6 +474,11 @@ def cpu_per_config(gpu_tflops):
         g = gpu_tflops.get(name)
         if g:
             row["gpu_over_cpu"] = round(g / tf, 1)
+        got = _gpu_rows(w, q, k, v, rows, heads)
+        err = np.abs(got - ref)
+        row["gpu_error"] = {"max_abs": float(err.max()), "mean_abs": float(err.mean()),
+                            "rel_fro": float(np.linalg.norm(got - ref) / np.linalg.norm(ref)),
+                            "pairs": int(rows.size)}
         out[name] = row
         print(f"[bench] oracle {name}: {sec:.2f} s per launch ({label})", file=sys.stderr, flush=True)
     w = workloads.WORKLOADS["480p"]
