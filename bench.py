@@ -601,7 +601,7 @@ def measured_peaks(attn_tflops):
     back to back, the second half averaged; the clock it implies at 4096 FLOP
     per CU and cycle; the same on zero operands, which do not toggle), the
     vendor library's 8192^3 bf16 product as a reference point, HBM reads
-    (2 GiB, far beyond the 256 MB Infinity Cache, best of three grid sizes),
+    (2 GiB, far beyond the 256 MB Infinity Cache, best of three run lengths),
     and LDS reads (16-byte and transposing 8-byte, at 8 waves per CU)."""
     import torch
     from paper_2606_06309_amd import binding as rf
@@ -641,7 +641,8 @@ def measured_peaks(attn_tflops):
     nbytes = 2 << 30
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     best = (0.0, 0)
-    for wgr in (1024, 2048, 4096):
+    # contiguous runs of 16 KB, 64 KB and 2 MB per workgroup of 1024 threads
+    for wgr in (nbytes // 16384, nbytes // 65536, 1024):
         sink = rf.rf_probe_hbm_read(src, wgr)
         torch.cuda.synchronize()
         ev = _events(5)
@@ -693,7 +694,8 @@ def measured_peaks(attn_tflops):
             "library_gemm_bf16": {"tflops": round(gemm_tf, 1), "shape": [8192, 8192, 8192],
                                   "call": "torch.matmul, random normal bf16"},
             "hbm_read": {"gbs": round(best[0], 1), "spec_gbs": PEAK_HBM_GBS,
-                         "frac_spec": round(best[0] / PEAK_HBM_GBS, 4), "bytes": nbytes, "workgroups": best[1]},
+                         "frac_spec": round(best[0] / PEAK_HBM_GBS, 4), "bytes": nbytes, "workgroups": best[1],
+                         "run_bytes": nbytes // best[1]},
             "lds_read": dict(lds, workgroups=lwg, rounds=lrounds, compute_units=cus),
             "attention_frac_of_measured_mfma": round(attn_tflops / mfma_tf, 4)}
 

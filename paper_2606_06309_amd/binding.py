@@ -667,12 +667,13 @@ def rf_probe_mfma_bf16(operands: torch.Tensor, workgroups: int, rounds: int, sin
 
 
 def rf_probe_hbm_read(src: torch.Tensor, workgroups: int, sink=None, stream=None):
-    """Enqueues the HBM read probe over src's bytes; returns the sink, int32
-    [workgroups * 256] whose XOR is the XOR of src's 32-bit words."""
+    """Enqueues the HBM read probe over src's bytes (workgroup w reads the
+    w-th of `workgroups` contiguous runs); returns the sink, int32
+    [workgroups] whose XOR is the XOR of src's 32-bit words."""
     if sink is None:
-        sink = _empty(workgroups * PROBE_THREADS, torch.int32, src.device, stream)
-    if sink.element_size() != 4 or sink.numel() < workgroups * PROBE_THREADS:
-        raise ValueError("sink must have 4-byte elements, workgroups * 256 of them")
+        sink = _empty(workgroups, torch.int32, src.device, stream)
+    if sink.element_size() != 4 or sink.numel() < workgroups:
+        raise ValueError("sink must have 4-byte elements, workgroups of them")
     _check(lib.rf_probe_hbm_read(_dev(src, "src"), src.numel() * src.element_size(), workgroups,
                                  _dev(sink, "sink"), _stream(stream)))
     return sink

@@ -15,8 +15,16 @@
 namespace rf {
 namespace {
 
-constexpr int kThreads = 512;
-constexpr int kUnroll = 2;
+// Launch shape: one wave per workgroup, one 16-byte vector per thread and
+// stream (the fastest of 64..512 threads x 1..4 vectors measured on MI355X).
+#ifndef RF_CACHE_THREADS
+#define RF_CACHE_THREADS 64
+#endif
+#ifndef RF_CACHE_UNROLL
+#define RF_CACHE_UNROLL 1
+#endif
+constexpr int kThreads = RF_CACHE_THREADS;
+constexpr int kUnroll = RF_CACHE_UNROLL;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ u32x4_t ld16(const u32x4_t *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st16(u32x4_t *p, u32x4_t v) { __builtin_nontemporal_store(v, p); }

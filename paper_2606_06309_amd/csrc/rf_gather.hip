@@ -12,8 +12,17 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 1024;   // one 16-byte vector per thread
-constexpr int kUnroll = 1;
+// Launch shape: one wave per workgroup copying 1 KB, one 16-byte vector per
+// thread (the fastest of 64..1024 threads x 1..4 vectors measured on MI355X:
+// many small workgroups keep more copies in flight than few large ones).
+#ifndef RF_COPY_THREADS
+#define RF_COPY_THREADS 64
+#endif
+#ifndef RF_COPY_UNROLL
+#define RF_COPY_UNROLL 1
+#endif
+constexpr int kThreads = RF_COPY_THREADS;
+constexpr int kUnroll = RF_COPY_UNROLL;
 
 struct CopyKArgs {
     const u32x4 *src;

@@ -149,8 +149,10 @@ struct SimParams {
 
 hipError_t launch_similarity(const SimParams &p, hipStream_t stream);
 
-// Device probes (measurement support): threads per workgroup of both probes.
+// Device probes (measurement support): threads per workgroup of the matrix and
+// LDS probes, and of the HBM read probe.
 constexpr int kProbeThreads = 256;
+constexpr int kHbmThreads = 1024;
 hipError_t launch_mfma_probe(const void *ops, int32_t workgroups, int32_t rounds, float *sink,
                              hipStream_t stream);
 hipError_t launch_lds_read_probe(int32_t workgroups, int32_t rounds, int32_t width, uint32_t *sink,

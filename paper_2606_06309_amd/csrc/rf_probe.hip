@@ -18,9 +18,12 @@
 //    the same loop sustained well under the rate the hardware reaches. The
 //    kernel is held to four waves per SIMD (114 registers) so that a grid of 4
 //    workgroups per CU runs in one round.
-//  * hbm_read_kernel: a grid-stride read of 16-byte words (four loads in
-//    flight per thread), folded with XOR into one 32-bit word per thread, so
-//    the XOR of all sink words equals the XOR of all words of the buffer.
+//  * hbm_read_kernel: workgroups of 1024 threads, each reading one contiguous
+//    run of the buffer in 16-byte words (four loads in flight per thread),
+//    folded with XOR into one 32-bit word per workgroup, so the XOR of all
+//    sink words equals the XOR of all words of the buffer. Runs of 16 KB (one
+//    word per thread) sustain the highest rate measured on MI355X; a grid
+//    stride over the whole buffer, or longer runs, read slower.
 //  * lds_read_kernel: every wave of a workgroup reads a 64 KB LDS array in
 //    full per round, with 16-byte reads or with the transposing 8-byte reads
 //    the attention kernel takes its V^T operands with, as many in flight as
@@ -74,20 +77,30 @@ void mfma_probe_kernel(const u32x4_t *ops, int32_t rounds, float *sink) {
     sink[static_cast<int64_t>(blockIdx.x) * kProbeThreads + threadIdx.x] = s;
 }
 
-__global__ __launch_bounds__(kProbeThreads) void hbm_read_kernel(const u32x4_t *src, int64_t n_words,
-                                                                 uint32_t *sink) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kProbeThreads;
-    int64_t i = static_cast<int64_t>(blockIdx.x) * kProbeThreads + threadIdx.x;
+__global__ __launch_bounds__(kHbmThreads) void hbm_read_kernel(const u32x4_t *src, int64_t n_words, int64_t per,
+                                                              uint32_t *sink) {
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per;
+    const int64_t b1 = b0 + per < n_words ? b0 + per : n_words;
     u32x4_t acc = {0u, 0u, 0u, 0u};
-    for (; i + 3 * stride < n_words; i += 4 * stride) {
+    int64_t i = b0 + threadIdx.x;
+    for (; i + 3 * kHbmThreads < b1; i += 4 * kHbmThreads) {
         const u32x4_t w0 = __builtin_nontemporal_load(src + i);
-        const u32x4_t w1 = __builtin_nontemporal_load(src + i + stride);
-        const u32x4_t w2 = __builtin_nontemporal_load(src + i + 2 * stride);
-        const u32x4_t w3 = __builtin_nontemporal_load(src + i + 3 * stride);
+        const u32x4_t w1 = __builtin_nontemporal_load(src + i + kHbmThreads);
+        const u32x4_t w2 = __builtin_nontemporal_load(src + i + 2 * kHbmThreads);
+        const u32x4_t w3 = __builtin_nontemporal_load(src + i + 3 * kHbmThreads);
         acc ^= (w0 ^ w1) ^ (w2 ^ w3);
     }
-    for (; i < n_words; i += stride) acc ^= src[i];
-    sink[static_cast<int64_t>(blockIdx.x) * kProbeThreads + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+    for (; i < b1; i += kHbmThreads) acc ^= src[i];
+    uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+    for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
+    __shared__ uint32_t red[kHbmThreads / 64];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t t = 0u;
+        for (int w = 0; w < kHbmThreads / 64; ++w) t ^= red[w];
+        sink[blockIdx.x] = t;
+    }
 }
 
 constexpr int kLdsWords = 16384;   // 64 KB of LDS per workgroup
@@ -172,8 +185,10 @@ hipError_t launch_mfma_probe(const void *ops, int32_t workgroups, int32_t rounds
 
 hipError_t launch_hbm_read_probe(const void *src, int64_t bytes, int32_t workgroups, uint32_t *sink,
                                  hipStream_t stream) {
-    hipLaunchKernelGGL(hbm_read_kernel, dim3(static_cast<uint32_t>(workgroups)), dim3(kProbeThreads), 0,
-                       stream, static_cast<const u32x4_t *>(src), bytes / 16, sink);
+    const int64_t n_words = bytes / 16;
+    const int64_t per = (n_words + workgroups - 1) / workgroups;
+    hipLaunchKernelGGL(hbm_read_kernel, dim3(static_cast<uint32_t>(workgroups)), dim3(kHbmThreads), 0,
+                       stream, static_cast<const u32x4_t *>(src), n_words, per, sink);
     return hipGetLastError();
 }
 

@@ -12,10 +12,17 @@
 namespace rf {
 namespace {
 
-// 512 threads x 2 vectors per workgroup and streaming (nontemporal) 16-byte
-// accesses: each byte is touched once, so nothing is kept in the caches.
-constexpr int kThreads = 512;
-constexpr int kUnroll = 2;
+// Launch shape (measured on MI355X against 64..1024 threads and 1..4 vectors per
+// thread): 128 threads x 2 vectors per workgroup, streaming (nontemporal)
+// 16-byte accesses, since each byte is touched once.
+#ifndef RF_PROJ_THREADS
+#define RF_PROJ_THREADS 128
+#endif
+#ifndef RF_PROJ_UNROLL
+#define RF_PROJ_UNROLL 2
+#endif
+constexpr int kThreads = RF_PROJ_THREADS;
+constexpr int kUnroll = RF_PROJ_UNROLL;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ u32x4_t ld16(const u32x4_t *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st16(u32x4_t *p, u32x4_t v) { __builtin_nontemporal_store(v, p); }

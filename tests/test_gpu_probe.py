@@ -70,8 +70,8 @@ def test_mfma_probe_random_operands_close():
     assert np.allclose(got, want, rtol=1e-4, atol=1e-2)
 
 
-@pytest.mark.parametrize("nbytes,wg", [(16, 1), (48, 3), (4096 * 16 + 48, 7), ((8 << 20) + 16 * 5, 64),
-                                       (64 << 20, 1024)])
+@pytest.mark.parametrize("nbytes,wg", [(16, 1), (48, 3), (48, 5), (4096 * 16 + 48, 7), ((8 << 20) + 16 * 5, 64),
+                                       (64 << 20, 1024), (64 << 20, 4096)])
 def test_hbm_read_probe_xor(nbytes, wg):
     print(f"[case] hbm read probe bytes={nbytes} wg={wg}", flush=True)
     g = torch.Generator(device="cpu").manual_seed(nbytes)
