@@ -13,7 +13,8 @@
 //     workspace. fp32 latents of at most 64 frames whose planes are a
 //     multiple of 4 take gram_partial_dma_kernel instead: the chunk's frame
 //     rows stream from HBM into LDS through the load units, double-buffered.
-//     About 512 workgroups in all (two per compute unit) cover the batch.
+//     At most 512 workgroups in all (one round at two per compute unit),
+//     at least one per batch element, cover the batch.
 //  2. gram_reduce_kernel: a workgroup per 4x4 block pair sums the partials of
 //     all runs in a fixed order (deterministic) into the output matrix.
 //  3. cosine_normalize_kernel: one workgroup per batch element turns G into
@@ -377,9 +378,11 @@ SimGeometry similarity_geometry(int32_t B, int32_t C, int32_t T, int64_t plane) 
     g.L = g.Tp <= kNarrowFrames ? kThreads : (L < kMaxChunk ? L : kMaxChunk);
     g.chunks_per_plane = (plane + g.L - 1) / g.L;
     g.n_chunks = static_cast<int64_t>(C) * g.chunks_per_plane;
-    // about kTargetWorkgroups workgroups over the whole batch, each a run of
+    // at most kTargetWorkgroups workgroups over the whole batch (one round at two
+    // per compute unit: a partly filled second round would double the time of
+    // the workgroups in it), at least one per batch element; each is a run of
     // chunks (one chunk per run when a thread has to walk several block pairs)
-    const int64_t per_b = (kTargetWorkgroups + B - 1) / B;
+    const int64_t per_b = kTargetWorkgroups / B > 0 ? kTargetWorkgroups / B : 1;
     g.run = g.Tp > kNarrowFrames ? 1 : (g.n_chunks + per_b - 1) / per_b;
     g.n_runs = (g.n_chunks + g.run - 1) / g.run;
     g.workspace_bytes = static_cast<int64_t>(B) * g.n_runs * g.NBP * 16 * static_cast<int64_t>(sizeof(double));
