@@ -617,8 +617,8 @@ int rf_probe_lds_read(int32_t workgroups, int32_t rounds, int32_t width, uint32_
  * contiguous run of words [w P, (w + 1) P), P = ceil(words / workgroups), and
  * writes the XOR of the 32-bit words it read to sink[w], so the XOR of
  * sink[0 .. workgroups) is the XOR of every 32-bit word of src. Bytes per
- * launch: `bytes`. Runs of 16 KB (workgroups = bytes / 16384) read fastest on
- * MI355X.
+ * launch: `bytes`. Runs of about 2 MB (workgroups = bytes / 2^21) read fastest
+ * on MI355X.
  * src: 16-byte aligned, bytes a positive multiple of 16. sink: device
  * uint32 [workgroups], 4-byte aligned. workgroups 1..2^20.
  * Errors: RF_ERR_INVALID_ARG (NULL, bytes), RF_ERR_RANGE (workgroups),

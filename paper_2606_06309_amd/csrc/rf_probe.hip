@@ -21,9 +21,10 @@
 //  * hbm_read_kernel: workgroups of 1024 threads, each reading one contiguous
 //    run of the buffer in 16-byte words (four loads in flight per thread),
 //    folded with XOR into one 32-bit word per workgroup, so the XOR of all
-//    sink words equals the XOR of all words of the buffer. Runs of 16 KB (one
-//    word per thread) sustain the highest rate measured on MI355X; a grid
-//    stride over the whole buffer, or longer runs, read slower.
+//    sink words equals the XOR of all words of the buffer. Runs of about 2 MB
+//    read fastest here (about 7 TB/s on MI355X); a grid stride over the whole
+//    buffer reads slower, and runs of 16 KB pay the workgroup's closing
+//    reduction for every 16 KB.
 //  * lds_read_kernel: every wave of a workgroup reads a 64 KB LDS array in
 //    full per round, with 16-byte reads or with the transposing 8-byte reads
 //    the attention kernel takes its V^T operands with, as many in flight as
