@@ -51,11 +51,14 @@ def _nonkeys(w):
     return [f for f in range(w.T) if f not in w.keyframes]
 
 
+# frame sizes in 16-byte vectors against the kernels' 64-vector (one wave) blocks
 SMALL = [
-    workloads.WORKLOADS["tiny"],                                          # fp32, 2 x 64
-    workloads.custom(7, 6, 10, 1, 64, (0, 4), dtype="bf16", seed=31),     # 960 vectors a frame (ragged block)
-    workloads.custom(9, 5, 7, 2, 128, (0, 3, 8), dtype="bf16", seed=32),  # N = 35
-    workloads.WORKLOADS["small"],                                         # 12 x 128, 292.5 blocks a frame
+    workloads.WORKLOADS["tiny"],                                          # fp32, 2 x 64: 2048 vectors a frame
+    workloads.custom(7, 6, 10, 1, 64, (0, 4), dtype="bf16", seed=31),     # 480 vectors: 7.5 blocks
+    workloads.custom(9, 5, 7, 2, 128, (0, 3, 8), dtype="bf16", seed=32),  # N = 35: 1120 vectors, 17.5 blocks
+    workloads.WORKLOADS["small"],                                         # 12 x 128: 299,520 vectors a frame
+    workloads.custom(4, 1, 1, 1, 64, (0,), dtype="bf16", seed=33),        # one token: 8 vectors, under a block
+    workloads.custom(5, 1, 13, 1, 64, (0, 2), dtype="bf16", seed=34),     # 104 vectors: 1.6 blocks
 ]
 
 

@@ -165,3 +165,42 @@ def test_attention_then_scatter_pipeline():
     assert_parity(got[tok], ref, "bf16", "pipeline")
     others = np.setdiff1d(np.arange(w.S), tok)
     assert np.all(got[others] == 0)
+
+
+# --- workgroup boundaries of the launch shapes -------------------------------------------
+# The copy runs one wave per 1 KB (64 vectors of 16 bytes), the projection 256 vectors per
+# workgroup: frames and planes just under, at and over those sizes, and tiny ones.
+
+@pytest.mark.parametrize("rows,row_bytes", [(1, 16), (3, 16), (63, 16), (64, 16), (65, 16), (2, 1024),
+                                            (1, 1040), (127, 16)])
+def test_gather_scatter_frame_sizes_around_a_workgroup(rows, row_bytes):
+    T = 256
+    ids = list(range(0, T - 1, 3)) + [T - 1]   # every third frame and the last one
+    print(f"[case] gather/scatter rows={rows} row_bytes={row_bytes} T={T} M={len(ids)}", flush=True)
+    cols = row_bytes // 2
+    src = _random_bits(T * rows, cols, 45 + rows)
+    out = rf.rf_gather_frames(src, ids, T, rows)
+    dst = torch.full((T * rows, cols), 0x5A5A, dtype=torch.int16, device="cuda")
+    before = dst.cpu().numpy()
+    rf.rf_scatter_frames(out, dst, ids, T, rows)
+    torch.cuda.synchronize()
+    exp = oracle.gather_frames(src.cpu().numpy(), ids, rows)
+    assert np.array_equal(out.cpu().numpy(), exp)
+    assert np.array_equal(dst.cpu().numpy(), oracle.scatter_frames(exp, before, ids, rows))
+
+
+@pytest.mark.parametrize("plane", [4, 1020, 1024, 1028, 2048 + 4])
+def test_projection_planes_around_a_workgroup(plane):
+    """fp32 planes of plane elements (4 per vector): 256 vectors per workgroup."""
+    B, C, T = 2, 3, 5
+    print(f"[case] projection plane={plane}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(plane)
+    lat = torch.randn((B, 2, C, T, 1, plane), generator=g, device="cuda")
+    mask = np.array([1, 0, 0, 1, 0], dtype=np.uint8)
+    ts = (24.0, 21.0, 23.0)
+    out = rf.rf_project_latents(lat, ts, mask)
+    torch.cuda.synchronize()
+    exp = oracle.project_latents(lat.cpu(), B, C, T, 1, plane, ts, mask)
+    assert_parity(_f64(out), exp, "f32", f"plane {plane}")
+    # keyframe planes are slot 1 bit for bit
+    assert torch.equal(out[:, :, 0], lat[:, 1, :, 0]) and torch.equal(out[:, :, 3], lat[:, 1, :, 3])
